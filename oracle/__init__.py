@@ -1,0 +1,18 @@
+"""fp64 CPU oracle for the policy-gradient hot path — TEST INFRASTRUCTURE ONLY.
+
+Only tests/, __graft_entry__.smoke() and bench.py's cpu_baseline leg may import
+or call anything in this package.  The product path (the HIP library and its
+Python binding) never does, and shares no code with it.
+"""
+from .rl_oracle import (  # noqa: F401
+    AGG_SEQ,
+    AGG_TOKEN,
+    compact,
+    group_index,
+    group_advantage,
+    token_logprob,
+    token_weights,
+    surrogate,
+    pg_loss_fwd_bwd,
+    sampled_rows,
+)

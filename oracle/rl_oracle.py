@@ -1,0 +1,334 @@
+"""Plain fp64 reference of the per-token policy-gradient computation.
+
+TEST INFRASTRUCTURE ONLY: imported by tests/, __graft_entry__.smoke() and the
+cpu_baseline leg of bench.py, never by the product path.  It shares no code
+with the HIP library.
+
+Every quantity is evaluated from its definition in float64 with complete
+vocabulary rows of logits (no online/streaming softmax).  Rows of tokens are
+processed in blocks purely to bound memory; rows are independent.
+
+Passages followed (ClawGym II):
+  * Sec. 2.3.1, masked clipped PPO objective: token ratio
+    rho_t = pi_theta(a_t|s_t) / pi_old(a_t|s_t), binary mask M_t (1 for valid
+    policy-generated tokens), min(rho A, clip(rho, 1-eps, 1+eps) A).
+  * Sec. 2.3.2, GRPO: A_i = (R_i - mu_q) / (sigma_q + eps) with the population
+    (1/G) standard deviation; objective = 1/G sum over trajectories of the
+    masked token mean of the clipped surrogate.
+  * Sec. 3.2.3, tree GRPO: the group is the n rollouts of a task; the rollout's
+    advantage goes to each of its trainable tokens, shared-prefix tokens once.
+  * Sec. 3.2.4: pi_old is a separate forward pass of the trainer (the log-prob
+    forward computed here).
+  * Sec. 3.3: under mix-harness training a group is a task-harness pair.
+  * Sec. 3.4: rollouts with sandbox failures leave both advantage estimation
+    and policy optimization.
+
+Readings where the paper is silent (each one is stated where it is applied):
+  * loss = - objective (the equations are objectives to maximise);
+  * default aggregation "seq": per-rollout masked token mean, 1/G_q within a
+    group, then the mean over the Q groups of the batch; alternative "token":
+    one masked token mean over the batch (the hat-E_t form of the PPO equation);
+  * advantage eps defaults to 1e-6; a group whose rewards are all bitwise equal
+    gets advantage exactly 0 (so does a group of one);
+  * asymmetric clip range [1 - eps_low, 1 + eps_high]; at rho exactly on a clip
+    bound the gradient passes (clipped only on strict inequality);
+  * optional entropy bonus: objective += c_ent * H_t under the same mask and
+    aggregation, H_t the full-vocabulary Shannon entropy in nats;
+  * the KL term and truncated importance sampling are off (beta = 0, w_t = 1);
+  * a rollout with no policy tokens contributes 0 to its group's sum but still
+    counts in G_q and in mu/sigma;
+  * group_id < 0 marks an excluded rollout: removed from mu, sigma, G_q, Q and
+    the loss; group ids are opaque keys, dense index = rank among the sorted
+    distinct non-negative ids;
+  * logits z = W h (no bias, temperature 1);
+  * norm_override replaces Q (seq) or the policy-token count (token), so
+    gradients of separately processed micro-batches add up to the one-call
+    gradient;
+  * with nothing to train (no policy tokens or every rollout excluded) the
+    loss is 0, dhidden is 0 and the overwritten dW is 0.
+"""
+from __future__ import annotations
+
+import numpy as np
+
+AGG_SEQ = 0
+AGG_TOKEN = 1
+
+
+def _f64(a):
+    return np.asarray(a, dtype=np.float64)
+
+
+# --------------------------------------------------------------------------
+# Token compaction and rollout segmentation (Sec. 2.3.1 mask, Sec. 3.2.3
+# per-rollout token count, Sec. 3.4 exclusion).
+# --------------------------------------------------------------------------
+def compact(mask, cu_seqlens, group_ids=None):
+    """Ascending positions t with M_t = 1 inside non-excluded rollouts.
+
+    Returns (idx int64 [N_eff], tok_rollout int64 [N_eff], n_pol int64 [R]).
+    mask None means every token is a policy token.
+    """
+    cu = np.asarray(cu_seqlens, dtype=np.int64)
+    R = cu.shape[0] - 1
+    N = int(cu[-1])
+    t = np.arange(N, dtype=np.int64)
+    rollout_of = np.searchsorted(cu[1:], t, side="right")
+    keep = np.ones(N, dtype=bool) if mask is None else (np.asarray(mask)[:N] != 0)
+    if group_ids is not None:
+        gid = np.asarray(group_ids, dtype=np.int64)
+        keep &= gid[rollout_of] >= 0
+    idx = np.flatnonzero(keep).astype(np.int64)
+    tok_rollout = rollout_of[idx]
+    n_pol = np.bincount(tok_rollout, minlength=R).astype(np.int64)
+    return idx, tok_rollout, n_pol
+
+
+def group_index(group_ids):
+    """Dense group index per rollout (-1 if excluded) and the number of groups Q."""
+    gid = np.asarray(group_ids, dtype=np.int64)
+    valid = gid >= 0
+    gi = np.full(gid.shape[0], -1, dtype=np.int64)
+    uniq, inv = np.unique(gid[valid], return_inverse=True)
+    gi[valid] = inv
+    return gi, int(uniq.shape[0])
+
+
+def group_advantage(rewards, group_ids, adv_eps=1e-6):
+    """GRPO advantage per rollout (Sec. 2.3.2 / Sec. 3.2.3), fp64.
+
+    Returns dict(adv [R], group_index [R], n_groups, G [Q], mu [Q], sigma [Q]).
+    """
+    r = _f64(rewards)
+    gi, Q = group_index(group_ids)
+    adv = np.zeros(r.shape[0], dtype=np.float64)
+    G = np.zeros(Q, dtype=np.int64)
+    mu = np.zeros(Q)
+    sigma = np.zeros(Q)
+    for q in range(Q):
+        members = np.flatnonzero(gi == q)
+        Rq = r[members]
+        n = members.shape[0]
+        G[q] = n
+        mu[q] = Rq.sum() / n
+        sigma[q] = np.sqrt(((Rq - mu[q]) ** 2).sum() / n)
+        if Rq.max() == Rq.min():
+            adv[members] = 0.0          # all-equal group: exactly 0
+        else:
+            adv[members] = (Rq - mu[q]) / (sigma[q] + adv_eps)
+    return dict(adv=adv, group_index=gi, n_groups=Q, G=G, mu=mu, sigma=sigma)
+
+
+# --------------------------------------------------------------------------
+# Log-prob forward (Sec. 3.2.4) with full-row logits.
+# --------------------------------------------------------------------------
+def _logits(h_rows, W):
+    return _f64(h_rows) @ _f64(W).T
+
+
+def token_logprob(h_rows, W, y, block: int = 256):
+    """log pi(y_t | s_t), entropy and log-partition per row, from complete logit rows.
+
+    z = W h_t; lse = max z + log sum exp(z - max z); logp = z_y - lse;
+    H = -sum_j p_j log p_j with log p_j = z_j - lse.
+    """
+    W64 = _f64(W)
+    y = np.asarray(y, dtype=np.int64)
+    n = y.shape[0]
+    lse = np.empty(n)
+    logp = np.empty(n)
+    H = np.empty(n)
+    for b0 in range(0, n, block):
+        b1 = min(n, b0 + block)
+        z = _f64(h_rows[b0:b1]) @ W64.T
+        m = z.max(axis=1)
+        l = m + np.log(np.exp(z - m[:, None]).sum(axis=1))
+        lp = z - l[:, None]
+        p = np.exp(lp)
+        lse[b0:b1] = l
+        logp[b0:b1] = lp[np.arange(b1 - b0), y[b0:b1]]
+        H[b0:b1] = -(p * lp).sum(axis=1)
+    return lse, logp, H
+
+
+# --------------------------------------------------------------------------
+# Clipped surrogate (Sec. 2.3.1 / 2.3.2) and aggregation weights.
+# --------------------------------------------------------------------------
+def surrogate(logp, old_logp, adv_tok, eps_low, eps_high):
+    """s_t = min(rho A, clip(rho, 1-eps_low, 1+eps_high) A) and the gradient gate.
+
+    Returns (s, rho, clipped) where clipped marks tokens whose surrogate does
+    not depend on rho (strict inequality beyond the bound on the side that the
+    min selects).
+    """
+    rho = np.exp(_f64(logp) - _f64(old_logp))
+    A = _f64(adv_tok)
+    c = np.clip(rho, 1.0 - eps_low, 1.0 + eps_high)
+    s = np.minimum(rho * A, c * A)
+    clipped = ((A > 0) & (rho > 1.0 + eps_high)) | ((A < 0) & (rho < 1.0 - eps_low))
+    return s, rho, clipped
+
+
+def token_weights(tok_rollout, n_pol, gi, G, n_groups, agg=AGG_SEQ, norm_override=None):
+    """d loss / d (s_t + c H_t) per compacted token (negative: loss = -objective).
+
+    seq:   -1 / (Q * G_q * n_r)   (per-rollout token mean, 1/G_q, mean over groups)
+    token: -1 / sum_t M_t
+    """
+    tok_rollout = np.asarray(tok_rollout, dtype=np.int64)
+    n = tok_rollout.shape[0]
+    if n == 0:
+        return np.zeros(0)
+    if agg == AGG_SEQ:
+        Qn = float(n_groups) if not norm_override else float(norm_override)
+        q = gi[tok_rollout]
+        return -1.0 / (Qn * G[q].astype(np.float64) * n_pol[tok_rollout].astype(np.float64))
+    Mn = float(n) if not norm_override else float(norm_override)
+    return np.full(n, -1.0 / Mn)
+
+
+def _aggregate(val, tok_rollout, n_pol, gi, G, n_groups, R, agg, norm_override):
+    """Objective J from per-token values val_t = s_t + c H_t (definitions above)."""
+    n = val.shape[0]
+    if n == 0 or n_groups == 0:
+        return 0.0
+    if agg == AGG_SEQ:
+        ell = np.zeros(R)
+        for r in range(R):
+            if gi[r] >= 0 and n_pol[r] > 0:
+                ell[r] = val[tok_rollout == r].sum() / n_pol[r]
+        J = 0.0
+        for q in range(n_groups):
+            J += ell[gi == q].sum() / G[q]
+        Qn = float(n_groups) if not norm_override else float(norm_override)
+        return J / Qn
+    Mn = float(n) if not norm_override else float(norm_override)
+    return val.sum() / Mn
+
+
+# --------------------------------------------------------------------------
+# Full forward + backward.
+# --------------------------------------------------------------------------
+def pg_loss_fwd_bwd(h, W, targets, mask, cu_seqlens, old_logp, rewards, group_ids, *,
+                    eps_low=0.2, eps_high=0.2, adv_eps=1e-6, entropy_coef=0.0, agg=AGG_SEQ,
+                    norm_override=None, grads=True, block: int = 128):
+    """Loss, per-token outputs and gradients w.r.t. hidden states and the LM-head weight.
+
+    h [N, d], W [V, d] (any float dtype, evaluated in fp64), targets [N], mask [N]
+    (None = all policy), cu_seqlens [R+1], old_logp [N], rewards [R], group_ids [R].
+    """
+    h = np.asarray(h)
+    W64 = _f64(W)
+    N, d = h.shape
+    V = W64.shape[0]
+    targets = np.asarray(targets, dtype=np.int64)
+    old = _f64(old_logp)
+    R = np.asarray(cu_seqlens).shape[0] - 1
+
+    idx, tok_r, n_pol = compact(mask, cu_seqlens, group_ids)
+    ga = group_advantage(rewards, group_ids, adv_eps)
+    adv, gi, Q, G = ga["adv"], ga["group_index"], ga["n_groups"], ga["G"]
+    n = idx.shape[0]
+    omega = token_weights(tok_r, n_pol, gi, G, Q, agg, norm_override)
+
+    lse = np.zeros(n)
+    logp = np.zeros(n)
+    H = np.zeros(n)
+    s = np.zeros(n)
+    rho = np.zeros(n)
+    clipped = np.zeros(n, dtype=bool)
+    g = np.zeros(n)
+    e = np.zeros(n)
+    dh = np.zeros((N, d)) if grads else None
+    dW = np.zeros((V, d)) if grads else None
+    for b0 in range(0, n, block):
+        b1 = min(n, b0 + block)
+        rows = idx[b0:b1]
+        hb = _f64(h[rows])
+        z = hb @ W64.T
+        m = z.max(axis=1)
+        l = m + np.log(np.exp(z - m[:, None]).sum(axis=1))
+        lp = z - l[:, None]
+        p = np.exp(lp)
+        yb = targets[rows]
+        ar = np.arange(b1 - b0)
+        lse[b0:b1] = l
+        logp[b0:b1] = lp[ar, yb]
+        H[b0:b1] = -(p * lp).sum(axis=1)
+        sb, rb, cb = surrogate(logp[b0:b1], old[rows], adv[tok_r[b0:b1]], eps_low, eps_high)
+        s[b0:b1], rho[b0:b1], clipped[b0:b1] = sb, rb, cb
+        # chain rule: dL/dlogp_t = omega_t A rho_t [not clipped]; dL/dH_t = omega_t c_ent
+        gb = omega[b0:b1] * adv[tok_r[b0:b1]] * rb * (~cb)
+        eb = omega[b0:b1] * entropy_coef
+        g[b0:b1], e[b0:b1] = gb, eb
+        if grads:
+            onehot = np.zeros_like(z)
+            onehot[ar, yb] = 1.0
+            # d logp_y / dz_j = [j = y] - p_j ;  d H / dz_j = -p_j (log p_j + H)
+            dz = gb[:, None] * (onehot - p) - eb[:, None] * p * (lp + H[b0:b1, None])
+            dh[rows] = dz @ W64
+            dW += dz.T @ hb
+
+    val = s + entropy_coef * H
+    J = _aggregate(val, tok_r, n_pol, gi, G, Q, R, agg, norm_override)
+    Jpg = _aggregate(s, tok_r, n_pol, gi, G, Q, R, agg, norm_override)
+    stats = dict(
+        loss=-J, pg_loss=-Jpg,
+        entropy_mean=float(H.mean()) if n else 0.0,
+        clip_frac=float(clipped.mean()) if n else 0.0,
+        ratio_mean=float(rho.mean()) if n else 0.0,
+        n_policy_tokens=int(n), n_groups=int(Q), n_valid_rollouts=int((gi >= 0).sum()))
+    logp_full = np.zeros(N)
+    H_full = np.zeros(N)
+    lse_full = np.zeros(N)
+    logp_full[idx] = logp
+    H_full[idx] = H
+    lse_full[idx] = lse
+    return dict(loss=-J, pg_loss=-Jpg, stats=stats, idx=idx, tok_rollout=tok_r, n_pol=n_pol,
+                adv=adv, group_index=gi, n_groups=Q, omega=omega, lse=lse, logp=logp, H=H,
+                rho=rho, clipped=clipped, g=g, e=e, logp_full=logp_full, entropy_full=H_full,
+                lse_full=lse_full, dh=dh, dW=dW)
+
+
+def sampled_rows(h_rows, W, y_rows, old_rows, adv_rows, omega_rows, *, eps_low, eps_high,
+                 entropy_coef=0.0, block: int = 64):
+    """Per-row forward and dhidden for selected policy rows of a large batch.
+
+    A row's log-prob, entropy and dhidden depend only on that row and on
+    per-rollout scalars (advantage, aggregation weight), so each can be checked
+    exactly without the rest of the batch.
+    """
+    W64 = _f64(W)
+    y = np.asarray(y_rows, dtype=np.int64)
+    n = y.shape[0]
+    out = {k: np.zeros(n) for k in ("lse", "logp", "H", "rho", "g", "e")}
+    out["clipped"] = np.zeros(n, dtype=bool)
+    out["dh"] = np.zeros((n, W64.shape[1]))
+    for b0 in range(0, n, block):
+        b1 = min(n, b0 + block)
+        hb = _f64(h_rows[b0:b1])
+        z = hb @ W64.T
+        m = z.max(axis=1)
+        l = m + np.log(np.exp(z - m[:, None]).sum(axis=1))
+        lp = z - l[:, None]
+        p = np.exp(lp)
+        ar = np.arange(b1 - b0)
+        lpy = lp[ar, y[b0:b1]]
+        Hb = -(p * lp).sum(axis=1)
+        A = _f64(adv_rows[b0:b1])
+        _, rb, cb = surrogate(lpy, old_rows[b0:b1], A, eps_low, eps_high)
+        om = _f64(omega_rows[b0:b1])
+        gb = om * A * rb * (~cb)
+        eb = om * entropy_coef
+        onehot = np.zeros_like(z)
+        onehot[ar, y[b0:b1]] = 1.0
+        dz = gb[:, None] * (onehot - p) - eb[:, None] * p * (lp + Hb[:, None])
+        out["lse"][b0:b1] = l
+        out["logp"][b0:b1] = lpy
+        out["H"][b0:b1] = Hb
+        out["rho"][b0:b1] = rb
+        out["clipped"][b0:b1] = cb
+        out["g"][b0:b1] = gb
+        out["e"][b0:b1] = eb
+        out["dh"][b0:b1] = dz @ W64
+    return out
