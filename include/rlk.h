@@ -1,0 +1,191 @@
+/*
+ * rlk — policy-gradient hot path of black-box agentic RL on MI355X (gfx950).
+ *
+ * The computation (ClawGym II, Sec. 2.3 and 3.2):
+ *   z_t = W h_t over the whole vocabulary (LM-head projection),
+ *   log pi(y_t|s_t) = z_{t,y_t} - logsumexp(z_t), entropy H_t of softmax(z_t),
+ *   group-relative advantage A_i = (R_i - mu_q)/(sigma_q + eps) over the rollouts of a
+ *   task (or task-harness pair) with the population std (Sec. 2.3.2, Sec. 3.2.3, Sec. 3.3),
+ *   the masked clipped surrogate min(rho A, clip(rho, 1-eps_lo, 1+eps_hi) A) with
+ *   rho = exp(logp - old_logp) and binary mask M_t (Sec. 2.3.1, masked GRPO objective of
+ *   Sec. 2.3.2), and its gradients dL/dhidden and dL/dW.
+ *
+ * Conventions shared by every entry point
+ *   - Every tensor pointer is a DEVICE pointer unless stated otherwise; row-major layout.
+ *   - hidden [N, d], W [V, d] and dhidden [N, d] use the batch dtype (fp32 or bf16).
+ *     Rows must be 16-byte aligned: d must be a multiple of 8.
+ *   - targets[t] is the token sampled at position t, already aligned with hidden[t] (no
+ *     shift inside); on policy rows it must lie in [0, V); on other rows it is ignored.
+ *   - mask[t] = 1 marks a policy-generated token (trained); 0 marks harness/tool tokens.
+ *     NULL means every token is a policy token.
+ *   - cu_seqlens [R+1] (device int32) packs rollouts back to back: rollout r owns
+ *     positions [cu[r], cu[r+1]); cu[0] = 0, cu[R] = N, non-decreasing.
+ *   - group_ids [R] are opaque int32 keys; rollouts sharing a key form one group.
+ *     A negative key excludes the rollout from advantage estimation and from the loss
+ *     (sandbox failures, Sec. 3.4).
+ *   - Ownership: the caller owns every buffer including the workspace; the library never
+ *     allocates or frees device memory on any call below.
+ *   - Streams: all work is enqueued on `stream` (a hipStream_t; NULL = the null stream).
+ *     Calls return without synchronising; outputs are valid once the stream reaches the
+ *     point of the call.  Concurrent calls must use distinct workspaces.
+ *   - Errors: invalid arguments are reported synchronously before anything is launched
+ *     (RLK_EINVAL, RLK_ESHAPE, RLK_EDTYPE, RLK_EWORKSPACE); a failed launch returns
+ *     RLK_EHIP.  Errors in device-resident data (out-of-range target on a policy row,
+ *     malformed cu_seqlens) cannot be seen by the host without a sync; kernels stay in
+ *     bounds, set bits in a status word held in the workspace, and rlk_check_status()
+ *     reports them.  Setting the environment variable RLK_DEBUG_SYNC=1 makes every call
+ *     synchronise and check that word.  rlk_last_error() describes the last failure of
+ *     the calling thread.
+ */
+#ifndef RLK_H
+#define RLK_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define RLK_VERSION 1
+
+typedef int32_t rlk_status_t;
+enum {
+  RLK_OK = 0,
+  RLK_EINVAL = 1,     /* null pointer or out-of-range scalar argument */
+  RLK_ESHAPE = 2,     /* inconsistent or unsupported sizes */
+  RLK_EDTYPE = 3,     /* unknown dtype */
+  RLK_EWORKSPACE = 4, /* workspace missing, misaligned or too small */
+  RLK_EHIP = 5,       /* a HIP runtime call or kernel launch failed */
+  RLK_EDATA = 6       /* device data error found by rlk_check_status */
+};
+
+enum { RLK_DTYPE_F32 = 0, RLK_DTYPE_BF16 = 1 };
+
+/* Token aggregation of the objective.
+ * SEQ_MEAN_TOKEN_MEAN (default, the masked GRPO objective of Sec. 2.3.2 with the
+ *   tree rule of Sec. 3.2.3): per-rollout masked token mean, 1/G_q over the rollouts of
+ *   a group, then the mean over the Q groups of the batch.
+ * TOKEN_MEAN (the hat-E_t form of Sec. 2.3.1): one masked token mean over the batch. */
+enum { RLK_AGG_SEQ_MEAN_TOKEN_MEAN = 0, RLK_AGG_TOKEN_MEAN = 1 };
+
+/* Bits of the device status word (rlk_check_status). */
+enum {
+  RLK_DERR_TARGET = 1,     /* a policy row's target lies outside [0, V) */
+  RLK_DERR_CU_SEQLENS = 2  /* cu[0] != 0, cu decreasing, or cu[R] != N */
+};
+
+typedef struct {
+  int64_t N;                  /* packed tokens (rows of hidden) */
+  int32_t R;                  /* rollouts */
+  int32_t d;                  /* hidden size, multiple of 8 */
+  int32_t V;                  /* vocabulary size */
+  int32_t dtype;              /* RLK_DTYPE_F32 or RLK_DTYPE_BF16 */
+  const int32_t* cu_seqlens;  /* device [R+1] */
+} rlk_batch_t;
+
+typedef struct {
+  float eps_low;        /* clip range [1 - eps_low, 1 + eps_high]; symmetric when equal */
+  float eps_high;
+  float adv_eps;        /* epsilon added to sigma_q; the paper leaves it unstated: 1e-6 */
+  float entropy_coef;   /* coefficient of an entropy bonus in the objective (0 = off) */
+  int32_t agg;          /* RLK_AGG_* */
+  int32_t accumulate_dW;/* 0: dW is overwritten; 1: the gradient is added to dW */
+  double norm_override; /* > 0: replaces Q (SEQ) or the policy-token count (TOKEN) so that
+                           micro-batched calls add up to the one-call gradient */
+  int64_t chunk_rows;   /* policy tokens per backward chunk, multiple of 256; 0 = auto */
+  int64_t reserved[4];  /* must be 0 */
+} rlk_pg_params_t;
+
+typedef struct {
+  float loss;             /* = *loss */
+  float pg_loss;          /* loss without the entropy term */
+  float entropy_mean;     /* token mean of H over policy tokens */
+  float clip_frac;        /* fraction of policy tokens whose surrogate is clipped */
+  float ratio_mean;       /* token mean of rho */
+  int32_t n_groups;       /* Q */
+  int32_t n_valid_rollouts;
+  int64_t n_policy_tokens;/* N_eff */
+} rlk_pg_stats_t;
+
+/* Workspace bytes needed by rlk_logprob_fwd (p == NULL) or by rlk_pg_loss_fwd_bwd (p
+ * != NULL) for this batch.  Host pointers; cu_seqlens is not read.  The workspace must
+ * be 256-byte aligned.  Returns RLK_ESHAPE for unsupported sizes. */
+rlk_status_t rlk_workspace_size(const rlk_batch_t* b, const rlk_pg_params_t* p, size_t* bytes);
+
+/* Workspace bytes needed by rlk_group_advantage for R rollouts. */
+rlk_status_t rlk_advantage_workspace_size(int32_t R, size_t* bytes);
+
+/* pi_old / pi_theta log-prob forward (Sec. 3.2.4: the trainer's own forward pass).
+ * For every row t with mask[t] = 1: logp[t] = log softmax(W h_t)[targets[t]],
+ * entropy[t] = H(softmax(W h_t)) in nats, lse[t] = logsumexp(W h_t).  Rows with
+ * mask 0 are written as 0.  entropy and lse may be NULL.  The logits are never stored:
+ * the log-softmax is taken online over vocabulary tiles. */
+rlk_status_t rlk_logprob_fwd(const rlk_batch_t* b, const void* hidden, const void* W,
+                             const int32_t* targets, const uint8_t* mask, float* logp,
+                             float* entropy, float* lse, void* ws, size_t ws_bytes,
+                             void* stream);
+
+/* Policy-token compaction and rollout segmentation (Sec. 2.3.1 mask; Sec. 3.2.3 per-rollout
+ * token count; Sec. 3.4 exclusion).  idx [N]: ascending positions t with mask[t] = 1 inside
+ * rollouts whose group id is >= 0 (group_ids NULL: no rollout is excluded), valid in its first
+ * *n_eff entries; tok_rollout [N]: the rollout of each such position; n_pol [R]: number of
+ * kept positions per rollout (0 for excluded rollouts); n_eff: device int32[1].  targets
+ * (optional) are checked on kept rows and flag RLK_DERR_TARGET.  Uses the workspace of
+ * rlk_logprob_fwd.  These are the gather lists through which every later operand is read. */
+rlk_status_t rlk_compact(const rlk_batch_t* b, const uint8_t* mask, const int32_t* group_ids,
+                         const int32_t* targets, int32_t* idx, int32_t* tok_rollout, int32_t* n_pol,
+                         int32_t* n_eff, void* ws, size_t ws_bytes, void* stream);
+
+/* Group-relative advantage (Sec. 2.3.2; tree GRPO, Sec. 3.2.3; task-harness groups,
+ * Sec. 3.3; exclusion, Sec. 3.4).  adv[r] = (R_r - mu_q)/(sigma_q + adv_eps) with mu, sigma
+ * the mean and population std of the non-excluded rewards of r's group; exactly 0 when
+ * every reward of the group is bitwise equal (including groups of one) and for excluded
+ * rollouts.  group_index[r] (optional) = rank of r's key among the sorted distinct
+ * non-negative keys, -1 if excluded; n_groups (optional, device int32[1]) = Q.
+ * Supports R <= 16384. */
+rlk_status_t rlk_group_advantage(int32_t R, const float* rewards, const int32_t* group_ids,
+                                 float adv_eps, float* adv, int32_t* group_index,
+                                 int32_t* n_groups, void* ws, size_t ws_bytes, void* stream);
+
+/* Masked clipped policy-gradient loss, forward and backward (Sec. 2.3.1-2.3.2,
+ * Sec. 3.2.3, Sec. 3.3, Sec. 3.4), with the log-prob forward inside.
+ *   loss      device float[1]: L = -objective under p->agg.
+ *   dhidden   [N, d] batch dtype: dL/dhidden; rows that are not trained are exactly 0.
+ *   dW        [V, d] fp32: dL/dW, overwritten or accumulated (p->accumulate_dW).
+ *   logp_out, entropy_out  [N] fp32 or NULL: per-token log-prob / entropy of the
+ *             current policy on trained rows, 0 elsewhere.
+ *   stats     device rlk_pg_stats_t or NULL.
+ * old_logp [N] fp32 is read on trained rows only.  With no trainable token the loss is 0,
+ * dhidden is 0 and an overwritten dW is 0. */
+rlk_status_t rlk_pg_loss_fwd_bwd(const rlk_batch_t* b, const void* hidden, const void* W,
+                                 const int32_t* targets, const uint8_t* mask,
+                                 const float* old_logp, const float* rewards,
+                                 const int32_t* group_ids, const rlk_pg_params_t* p,
+                                 float* loss, void* dhidden, float* dW, float* logp_out,
+                                 float* entropy_out, rlk_pg_stats_t* stats, void* ws,
+                                 size_t ws_bytes, void* stream);
+
+/* Synchronises `stream`, then reads the status word that the previous calls using `ws`
+ * left there.  *flags (optional host pointer) receives RLK_DERR_* bits; returns RLK_OK or
+ * RLK_EDATA.  Each entry point clears the word when it starts. */
+rlk_status_t rlk_check_status(const void* ws, void* stream, int32_t* flags);
+
+const char* rlk_status_string(rlk_status_t s);
+const char* rlk_last_error(void);
+int32_t rlk_version(void);
+
+/* Kernel timing for measurement.  Between rlk_profile_begin() and rlk_profile_end() every
+ * kernel launch of the entry points above is bracketed by a pair of HIP events on the
+ * call's stream.  rlk_profile_end() waits for them and fills, per kernel kind k < *n_kinds
+ * (host arrays of length max_kinds), the summed milliseconds and the launch count. */
+rlk_status_t rlk_profile_begin(void);
+rlk_status_t rlk_profile_end(int32_t max_kinds, double* total_ms, int32_t* launches,
+                             int32_t* n_kinds);
+const char* rlk_kernel_kind_name(int32_t kind);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* RLK_H */

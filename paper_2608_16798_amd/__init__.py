@@ -1,0 +1,276 @@
+"""Python binding of librlk (the MI355X policy-gradient hot path).
+
+Argument marshalling only: every step of the computation runs in the HIP kernels of
+librlk.so, reached through its C ABI (include/rlk.h) with ctypes.  torch provides
+device memory and streams.  There is no fallback: if the library is missing or no
+GPU is present, the calls raise.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional
+
+PKG_DIR = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(PKG_DIR, "librlk.so")
+
+RLK_OK, RLK_EINVAL, RLK_ESHAPE, RLK_EDTYPE, RLK_EWORKSPACE, RLK_EHIP, RLK_EDATA = range(7)
+DTYPE_F32, DTYPE_BF16 = 0, 1
+AGG_SEQ, AGG_TOKEN = 0, 1
+DERR_TARGET, DERR_CU_SEQLENS = 1, 2
+
+EXPORTS = [
+    "rlk_workspace_size", "rlk_advantage_workspace_size", "rlk_compact", "rlk_logprob_fwd", "rlk_group_advantage",
+    "rlk_pg_loss_fwd_bwd", "rlk_check_status", "rlk_status_string", "rlk_last_error", "rlk_version",
+    "rlk_profile_begin", "rlk_profile_end", "rlk_kernel_kind_name",
+]
+
+
+class Batch(ctypes.Structure):
+    _fields_ = [("N", ctypes.c_int64), ("R", ctypes.c_int32), ("d", ctypes.c_int32), ("V", ctypes.c_int32),
+                ("dtype", ctypes.c_int32), ("cu_seqlens", ctypes.c_void_p)]
+
+
+class PgParams(ctypes.Structure):
+    _fields_ = [("eps_low", ctypes.c_float), ("eps_high", ctypes.c_float), ("adv_eps", ctypes.c_float),
+                ("entropy_coef", ctypes.c_float), ("agg", ctypes.c_int32), ("accumulate_dW", ctypes.c_int32),
+                ("norm_override", ctypes.c_double), ("chunk_rows", ctypes.c_int64),
+                ("reserved", ctypes.c_int64 * 4)]
+
+
+class PgStats(ctypes.Structure):
+    _fields_ = [("loss", ctypes.c_float), ("pg_loss", ctypes.c_float), ("entropy_mean", ctypes.c_float),
+                ("clip_frac", ctypes.c_float), ("ratio_mean", ctypes.c_float), ("n_groups", ctypes.c_int32),
+                ("n_valid_rollouts", ctypes.c_int32), ("n_policy_tokens", ctypes.c_int64)]
+
+
+class RlkError(RuntimeError):
+    def __init__(self, code: int, msg: str):
+        super().__init__(f"rlk error {code}: {msg}")
+        self.code = code
+
+
+_lib = None
+
+
+def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
+    """Load librlk.so (raises if it has not been built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise RuntimeError(f"librlk.so not found at {path}; build it with `python -m paper_2608_16798_amd.build`")
+    lib = ctypes.CDLL(path)
+    vp, i32, i64, sz, f32 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t, ctypes.c_float
+    pb, pp = ctypes.POINTER(Batch), ctypes.POINTER(PgParams)
+    lib.rlk_workspace_size.argtypes = [pb, pp, ctypes.POINTER(sz)]
+    lib.rlk_advantage_workspace_size.argtypes = [i32, ctypes.POINTER(sz)]
+    lib.rlk_compact.argtypes = [pb, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
+    lib.rlk_logprob_fwd.argtypes = [pb, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
+    lib.rlk_group_advantage.argtypes = [i32, vp, vp, f32, vp, vp, vp, vp, sz, vp]
+    lib.rlk_pg_loss_fwd_bwd.argtypes = [pb, vp, vp, vp, vp, vp, vp, vp, pp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
+    lib.rlk_check_status.argtypes = [vp, vp, ctypes.POINTER(i32)]
+    lib.rlk_status_string.argtypes = [i32]
+    lib.rlk_status_string.restype = ctypes.c_char_p
+    lib.rlk_last_error.argtypes = []
+    lib.rlk_last_error.restype = ctypes.c_char_p
+    lib.rlk_version.restype = i32
+    lib.rlk_profile_begin.argtypes = []
+    lib.rlk_profile_end.argtypes = [i32, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(i32), ctypes.POINTER(i32)]
+    lib.rlk_kernel_kind_name.argtypes = [i32]
+    lib.rlk_kernel_kind_name.restype = ctypes.c_char_p
+    for name in EXPORTS:
+        if name not in ("rlk_status_string", "rlk_last_error", "rlk_kernel_kind_name", "rlk_version"):
+            getattr(lib, name).restype = i32
+    _lib = lib
+    return lib
+
+
+def _check(code: int):
+    if code != RLK_OK:
+        raise RlkError(code, load_library().rlk_last_error().decode())
+
+
+def _ptr(t) -> Optional[int]:
+    return None if t is None else t.data_ptr()
+
+
+def _stream_handle(stream) -> Optional[int]:
+    import torch
+
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return s.cuda_stream
+
+
+def _dtype_code(t) -> int:
+    import torch
+
+    if t.dtype == torch.bfloat16:
+        return DTYPE_BF16
+    if t.dtype == torch.float32:
+        return DTYPE_F32
+    raise TypeError(f"unsupported dtype {t.dtype}")
+
+
+def make_batch(hidden, W, cu_seqlens) -> Batch:
+    N, d = hidden.shape
+    V = W.shape[0]
+    R = cu_seqlens.shape[0] - 1
+    return Batch(N=N, R=R, d=d, V=V, dtype=_dtype_code(W), cu_seqlens=_ptr(cu_seqlens))
+
+
+def make_params(eps_low=0.2, eps_high=None, adv_eps=1e-6, entropy_coef=0.0, agg=AGG_SEQ, accumulate_dW=False,
+                norm_override=0.0, chunk_rows=0) -> PgParams:
+    p = PgParams()
+    p.eps_low = eps_low
+    p.eps_high = eps_low if eps_high is None else eps_high
+    p.adv_eps = adv_eps
+    p.entropy_coef = entropy_coef
+    p.agg = agg
+    p.accumulate_dW = 1 if accumulate_dW else 0
+    p.norm_override = float(norm_override or 0.0)
+    p.chunk_rows = int(chunk_rows)
+    return p
+
+
+def workspace_size(batch: Batch, params: Optional[PgParams] = None) -> int:
+    lib = load_library()
+    n = ctypes.c_size_t()
+    _check(lib.rlk_workspace_size(ctypes.byref(batch), ctypes.byref(params) if params is not None else None,
+                                  ctypes.byref(n)))
+    return n.value
+
+
+def advantage_workspace_size(R: int) -> int:
+    lib = load_library()
+    n = ctypes.c_size_t()
+    _check(lib.rlk_advantage_workspace_size(R, ctypes.byref(n)))
+    return n.value
+
+
+def alloc_workspace(nbytes: int, device="cuda"):
+    """A 256-byte aligned uint8 device buffer of at least nbytes (torch allocations are)."""
+    import torch
+
+    ws = torch.empty(max(int(nbytes), 256), dtype=torch.uint8, device=device)
+    assert ws.data_ptr() % 256 == 0
+    return ws
+
+
+def logprob_fwd(hidden, W, targets, mask, cu_seqlens, logp=None, entropy=None, lse=None, ws=None, stream=None):
+    """Per-token log-prob / entropy / log-partition of the sampled tokens (rows with mask 0 -> 0)."""
+    import torch
+
+    lib = load_library()
+    b = make_batch(hidden, W, cu_seqlens)
+    N = b.N
+    dev = hidden.device
+    if logp is None:
+        logp = torch.empty(N, dtype=torch.float32, device=dev)
+    if ws is None:
+        ws = alloc_workspace(workspace_size(b), dev)
+    _check(lib.rlk_logprob_fwd(ctypes.byref(b), _ptr(hidden), _ptr(W), _ptr(targets), _ptr(mask), _ptr(logp),
+                               _ptr(entropy), _ptr(lse), _ptr(ws), ws.numel(), _stream_handle(stream)))
+    return logp, entropy, lse, ws
+
+
+def compact(cu_seqlens, mask, group_ids=None, targets=None, N=None, V=1, d=8, ws=None, stream=None):
+    """Compacted policy-token positions, their rollouts, per-rollout counts and N_eff (device tensors)."""
+    import torch
+
+    lib = load_library()
+    dev = cu_seqlens.device
+    R = cu_seqlens.shape[0] - 1
+    if N is None:
+        N = mask.shape[0]
+    b = Batch(N=N, R=R, d=d, V=V, dtype=DTYPE_BF16, cu_seqlens=_ptr(cu_seqlens))
+    idx = torch.empty(max(N, 1), dtype=torch.int32, device=dev)
+    tokr = torch.empty(max(N, 1), dtype=torch.int32, device=dev)
+    n_pol = torch.empty(max(R, 1), dtype=torch.int32, device=dev)
+    n_eff = torch.empty(1, dtype=torch.int32, device=dev)
+    if ws is None:
+        ws = alloc_workspace(workspace_size(b), dev)
+    _check(lib.rlk_compact(ctypes.byref(b), _ptr(mask), _ptr(group_ids), _ptr(targets), _ptr(idx), _ptr(tokr),
+                           _ptr(n_pol), _ptr(n_eff), _ptr(ws), ws.numel(), _stream_handle(stream)))
+    return idx, tokr, n_pol[:R], n_eff, ws
+
+
+def group_advantage(rewards, group_ids, adv_eps=1e-6, adv=None, group_index=None, n_groups=None, ws=None,
+                    stream=None):
+    import torch
+
+    lib = load_library()
+    R = rewards.shape[0]
+    dev = rewards.device
+    if adv is None:
+        adv = torch.empty(R, dtype=torch.float32, device=dev)
+    if ws is None:
+        ws = alloc_workspace(advantage_workspace_size(R), dev)
+    _check(lib.rlk_group_advantage(R, _ptr(rewards), _ptr(group_ids), adv_eps, _ptr(adv), _ptr(group_index),
+                                   _ptr(n_groups), _ptr(ws), ws.numel(), _stream_handle(stream)))
+    return adv
+
+
+def pg_loss_fwd_bwd(hidden, W, targets, mask, cu_seqlens, old_logp, rewards, group_ids, params: PgParams,
+                    loss=None, dhidden=None, dW=None, logp_out=None, entropy_out=None, stats=None, ws=None,
+                    stream=None):
+    """Loss, dL/dhidden and dL/dW of the masked clipped policy-gradient objective."""
+    import torch
+
+    lib = load_library()
+    b = make_batch(hidden, W, cu_seqlens)
+    dev = hidden.device
+    if loss is None:
+        loss = torch.empty(1, dtype=torch.float32, device=dev)
+    if dhidden is None:
+        dhidden = torch.empty_like(hidden)
+    if dW is None:
+        dW = torch.empty(W.shape, dtype=torch.float32, device=dev)
+    if ws is None:
+        ws = alloc_workspace(workspace_size(b, params), dev)
+    _check(lib.rlk_pg_loss_fwd_bwd(ctypes.byref(b), _ptr(hidden), _ptr(W), _ptr(targets), _ptr(mask),
+                                   _ptr(old_logp), _ptr(rewards), _ptr(group_ids), ctypes.byref(params), _ptr(loss),
+                                   _ptr(dhidden), _ptr(dW), _ptr(logp_out), _ptr(entropy_out), _ptr(stats),
+                                   _ptr(ws), ws.numel(), _stream_handle(stream)))
+    return loss, dhidden, dW, ws
+
+
+def check_status(ws, stream=None) -> int:
+    """Synchronises the stream and returns the device data-error bits left in ws."""
+    lib = load_library()
+    flags = ctypes.c_int32(0)
+    code = lib.rlk_check_status(_ptr(ws), _stream_handle(stream), ctypes.byref(flags))
+    if code not in (RLK_OK, RLK_EDATA):
+        _check(code)
+    return flags.value
+
+
+def stats_from_tensor(t) -> dict:
+    """Decodes a device buffer holding an rlk_pg_stats_t (as returned by stats_buffer())."""
+    raw = bytes(t.cpu().numpy().tobytes())
+    s = PgStats.from_buffer_copy(raw[:ctypes.sizeof(PgStats)])
+    return {f: getattr(s, f) for f, _ in PgStats._fields_}
+
+
+def stats_buffer(device="cuda"):
+    import torch
+
+    return torch.zeros(ctypes.sizeof(PgStats), dtype=torch.uint8, device=device)
+
+
+def profile_begin():
+    _check(load_library().rlk_profile_begin())
+
+
+def profile_end() -> dict:
+    lib = load_library()
+    n = 32
+    ms = (ctypes.c_double * n)()
+    cnt = (ctypes.c_int32 * n)()
+    nk = ctypes.c_int32()
+    _check(lib.rlk_profile_end(n, ms, cnt, ctypes.byref(nk)))
+    out = {}
+    for k in range(min(n, nk.value)):
+        if cnt[k]:
+            out[lib.rlk_kernel_kind_name(k).decode()] = (ms[k], cnt[k])
+    return out

@@ -1,0 +1,349 @@
+// Policy-token compaction, rollout segmentation and group-relative advantages.
+//
+// Compaction keeps the positions t with M_t = 1 (Sec. 2.3.1: only valid policy-generated
+// tokens are optimised) inside rollouts that are not excluded (Sec. 3.4: sandbox
+// failures leave advantage estimation and policy optimisation), in ascending order.  Every
+// later GEMM operand is gathered through this list, so masked tokens cost no MFMA work.
+// The per-rollout count of kept tokens is the normaliser of the per-rollout token mean
+// (masked GRPO objective, Sec. 2.3.2; shared-prefix tokens counted once, Sec. 3.2.3).
+//
+// Advantages follow the GRPO equation of Sec. 2.3.2 / Sec. 3.2.3: mean and population
+// std over the non-excluded rollouts of a group (a task-harness pair, Sec. 3.3), with
+// group keys treated as opaque and unordered.  All reductions run in a fixed order, in
+// fp64, so results are bitwise reproducible.
+#include "rlk_internal.h"
+
+namespace rlk {
+
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int kPerThread = kScanTile / kThreads;  // 16 tokens per thread
+
+__device__ inline int rollout_of(const int32_t* cu, int R, int64_t t) {
+  // first r with cu[r+1] > t, clamped to [0, R-1]; tolerant of malformed cu
+  int lo = 0, hi = R - 1;
+  while (lo < hi) {
+    int mid = (lo + hi) >> 1;
+    if ((int64_t)cu[mid + 1] > t) hi = mid; else lo = mid + 1;
+  }
+  return lo;
+}
+
+__device__ inline int wave_inclusive_scan(int v, int lane) {
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    int n = __shfl_up(v, o, 64);
+    if (lane >= o) v += n;
+  }
+  return v;
+}
+
+template <typename X>
+__device__ inline X wave_sum(X v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+
+__global__ void __launch_bounds__(kThreads) k_begin(WsHeader* hdr, const int32_t* cu, int R, int64_t N) {
+  __shared__ int err;
+  if (threadIdx.x == 0) err = 0;
+  __syncthreads();
+  int e = 0;
+  if (R > 0) {
+    for (int r = threadIdx.x; r < R; r += blockDim.x)
+      if (cu[r] > cu[r + 1]) e |= RLK_DERR_CU_SEQLENS;
+    if (threadIdx.x == 0 && (cu[0] != 0 || (int64_t)cu[R] != N)) e |= RLK_DERR_CU_SEQLENS;
+  }
+  if (e) atomicOr(&err, e);
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    hdr->status = err;
+    hdr->n_eff = 0;
+    hdr->n_groups = 0;
+    hdr->n_valid = 0;
+  }
+}
+
+__device__ inline bool keep_token(const uint8_t* mask, const int32_t* gid, int r, int64_t t) {
+  bool k = mask ? (mask[t] != 0) : true;
+  if (gid) k = k && (gid[r] >= 0);
+  return k;
+}
+
+__global__ void __launch_bounds__(kThreads)
+k_count(const uint8_t* mask, const int32_t* cu, const int32_t* gid, int R, int64_t N, uint8_t* keep,
+        int32_t* blkcnt) {
+  __shared__ int partial[kThreads / 64];
+  const int64_t t0 = (int64_t)blockIdx.x * kScanTile + (int64_t)threadIdx.x * kPerThread;
+  int cnt = 0;
+  if (t0 < N) {
+    int r = rollout_of(cu, R, t0);
+    for (int i = 0; i < kPerThread; ++i) {
+      int64_t t = t0 + i;
+      if (t >= N) break;
+      while (r < R - 1 && (int64_t)cu[r + 1] <= t) ++r;
+      bool k = keep_token(mask, gid, r, t);
+      keep[t] = k ? 1 : 0;
+      cnt += k ? 1 : 0;
+    }
+  }
+  cnt = wave_sum(cnt);
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  if (lane == 0) partial[w] = cnt;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    int s = 0;
+    for (int i = 0; i < kThreads / 64; ++i) s += partial[i];
+    blkcnt[blockIdx.x] = s;
+  }
+}
+
+__global__ void __launch_bounds__(1024) k_scan(const int32_t* blkcnt, int32_t* blkoff, int nblk, WsHeader* hdr) {
+  __shared__ int wsum[16];
+  __shared__ int carry_s;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  if (threadIdx.x == 0) carry_s = 0;
+  __syncthreads();
+  for (int base = 0; base < nblk; base += 1024) {
+    int i = base + threadIdx.x;
+    int v = i < nblk ? blkcnt[i] : 0;
+    int inc = wave_inclusive_scan(v, lane);
+    if (lane == 63) wsum[w] = inc;
+    __syncthreads();
+    int woff = 0;
+    for (int j = 0; j < w; ++j) woff += wsum[j];
+    int carry = carry_s;
+    if (i < nblk) blkoff[i] = carry + woff + inc - v;
+    __syncthreads();
+    if (threadIdx.x == 1023) carry_s = carry + woff + inc;
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) hdr->n_eff = carry_s;
+}
+
+__global__ void __launch_bounds__(kThreads)
+k_write_idx(const uint8_t* keep, const int32_t* cu, int R, int64_t N, const int32_t* blkoff,
+            const int32_t* targets, int V, int32_t* idx, int32_t* tokr, int32_t* ytgt, float* zy,
+            WsHeader* hdr) {
+  __shared__ int wsum[kThreads / 64];
+  const int64_t t0 = (int64_t)blockIdx.x * kScanTile + (int64_t)threadIdx.x * kPerThread;
+  int cnt = 0;
+  for (int i = 0; i < kPerThread; ++i) {
+    int64_t t = t0 + i;
+    if (t < N) cnt += keep[t];
+  }
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  int inc = wave_inclusive_scan(cnt, lane);
+  if (lane == 63) wsum[w] = inc;
+  __syncthreads();
+  int off = blkoff[blockIdx.x];
+  for (int j = 0; j < w; ++j) off += wsum[j];
+  off += inc - cnt;
+  if (cnt == 0) return;
+  int r = rollout_of(cu, R, t0);
+  int bad = 0;
+  for (int i = 0; i < kPerThread; ++i) {
+    int64_t t = t0 + i;
+    if (t >= N) break;
+    while (r < R - 1 && (int64_t)cu[r + 1] <= t) ++r;
+    if (keep[t]) {
+      const int y = targets ? targets[t] : 0;
+      if (y < 0 || y >= V) bad = 1;
+      idx[off] = (int32_t)t;
+      tokr[off] = r;
+      ytgt[off] = y;
+      zy[off] = 0.0f;
+      ++off;
+    }
+  }
+  if (bad) atomicOr(&hdr->status, RLK_DERR_TARGET);
+}
+
+__device__ inline int lower_bound_i32(const int32_t* a, int n, int64_t key) {
+  int lo = 0, hi = n;
+  while (lo < hi) {
+    int mid = (lo + hi) >> 1;
+    if ((int64_t)a[mid] < key) lo = mid + 1; else hi = mid;
+  }
+  return lo;
+}
+
+__global__ void __launch_bounds__(kThreads)
+k_rollout_offsets(const int32_t* cu, int R, int64_t N, const int32_t* idx, const WsHeader* hdr,
+                  int32_t* rstart, int32_t* rnpol) {
+  const int r = blockIdx.x * blockDim.x + threadIdx.x;
+  if (r >= R) return;
+  const int n = hdr->n_eff;
+  int64_t a = cu[r], b = cu[r + 1];
+  a = a < 0 ? 0 : (a > N ? N : a);
+  b = b < a ? a : (b > N ? N : b);
+  int s = lower_bound_i32(idx, n, a);
+  int e = lower_bound_i32(idx, n, b);
+  rstart[r] = s;
+  rnpol[r] = e - s;
+}
+
+// ---- group-relative advantages ----
+
+__global__ void __launch_bounds__(kThreads) k_group_first(const int32_t* gid, int R, int32_t* first) {
+  const int r = blockIdx.x * blockDim.x + threadIdx.x;
+  if (r >= R) return;
+  const int32_t key = gid[r];
+  int f = key >= 0 ? 1 : 0;
+  for (int j = 0; j < r && f; ++j)
+    if (gid[j] == key) f = 0;
+  first[r] = f;
+}
+
+__global__ void __launch_bounds__(kThreads)
+k_group_rank(const int32_t* gid, int R, const int32_t* first, int32_t* gidx, WsHeader* hdr) {
+  const int r = blockIdx.x * blockDim.x + threadIdx.x;
+  if (r < R) {
+    const int32_t key = gid[r];
+    int rank = -1;
+    if (key >= 0) {
+      rank = 0;
+      for (int j = 0; j < R; ++j) rank += (first[j] && gid[j] < key) ? 1 : 0;
+    }
+    gidx[r] = rank;
+  }
+  if (blockIdx.x == 0) {
+    __shared__ int sq[kThreads / 64], sv[kThreads / 64];
+    int q = 0, v = 0;
+    for (int j = threadIdx.x; j < R; j += blockDim.x) {
+      q += first[j];
+      v += gid[j] >= 0 ? 1 : 0;
+    }
+    q = wave_sum(q);
+    v = wave_sum(v);
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    if (lane == 0) { sq[w] = q; sv[w] = v; }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+      int a = 0, b = 0;
+      for (int i = 0; i < kThreads / 64; ++i) { a += sq[i]; b += sv[i]; }
+      hdr->n_groups = a;
+      hdr->n_valid = b;
+    }
+  }
+}
+
+// One wavefront per group: members visited in ascending rollout order, fixed shuffle tree.
+__global__ void __launch_bounds__(kThreads)
+k_group_stats(const float* rewards, const int32_t* gidx, int R, const WsHeader* hdr, int32_t* gsize,
+              double* gmu, double* gsig, int32_t* geq) {
+  const int lane = threadIdx.x & 63;
+  const int q = blockIdx.x * (kThreads / 64) + (threadIdx.x >> 6);
+  if (q >= hdr->n_groups) return;
+  double sum = 0.0;
+  int cnt = 0;
+  float mn = INFINITY, mx = -INFINITY;
+  for (int base = 0; base < R; base += 64) {
+    int r = base + lane;
+    if (r < R && gidx[r] == q) {
+      float v = rewards[r];
+      sum += (double)v;
+      cnt += 1;
+      mn = fminf(mn, v);
+      mx = fmaxf(mx, v);
+    }
+  }
+  sum = wave_sum(sum);
+  cnt = wave_sum(cnt);
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    mn = fminf(mn, __shfl_xor(mn, o, 64));
+    mx = fmaxf(mx, __shfl_xor(mx, o, 64));
+  }
+  const double mu = cnt > 0 ? sum / (double)cnt : 0.0;
+  double ss = 0.0;
+  for (int base = 0; base < R; base += 64) {
+    int r = base + lane;
+    if (r < R && gidx[r] == q) {
+      double dv = (double)rewards[r] - mu;
+      ss += dv * dv;
+    }
+  }
+  ss = wave_sum(ss);
+  if (lane == 0) {
+    gsize[q] = cnt;
+    gmu[q] = mu;
+    gsig[q] = cnt > 0 ? sqrt(ss / (double)cnt) : 0.0;
+    geq[q] = (mn == mx) ? 1 : 0;
+  }
+}
+
+__global__ void __launch_bounds__(kThreads)
+k_advantage(const float* rewards, const int32_t* gidx, int R, const double* gmu, const double* gsig,
+            const int32_t* geq, float adv_eps, float* adv) {
+  const int r = blockIdx.x * blockDim.x + threadIdx.x;
+  if (r >= R) return;
+  const int q = gidx[r];
+  double a = 0.0;
+  if (q >= 0 && !geq[q]) a = ((double)rewards[r] - gmu[q]) / (gsig[q] + (double)adv_eps);
+  adv[r] = (float)a;
+}
+
+inline dim3 blocks_for(int64_t n, int per) { return dim3((unsigned)((n + per - 1) / per)); }
+
+}  // namespace
+
+hipError_t launch_begin(int32_t* status_hdr, const int32_t* cu, int R, int64_t N, hipStream_t s) {
+  prof_mark(KK_BEGIN, true, s);
+  k_begin<<<1, kThreads, 0, s>>>(reinterpret_cast<WsHeader*>(status_hdr), cu, R, N);
+  prof_mark(KK_BEGIN, false, s);
+  return hipGetLastError();
+}
+
+hipError_t launch_compact(const uint8_t* mask, const int32_t* cu, const int32_t* gid, int R, int64_t N,
+                          const int32_t* targets, int V, char* ws, const WsLayout& L, hipStream_t s) {
+  WsHeader* hdr = reinterpret_cast<WsHeader*>(ws + L.hdr);
+  uint8_t* keep = reinterpret_cast<uint8_t*>(ws + L.keep);
+  int32_t* blkcnt = reinterpret_cast<int32_t*>(ws + L.blkcnt);
+  int32_t* blkoff = reinterpret_cast<int32_t*>(ws + L.blkoff);
+  if (N > 0) {
+    prof_mark(KK_COUNT, true, s);
+    k_count<<<L.nblk, kThreads, 0, s>>>(mask, cu, gid, R, N, keep, blkcnt);
+    prof_mark(KK_COUNT, false, s);
+    prof_mark(KK_SCAN, true, s);
+    k_scan<<<1, 1024, 0, s>>>(blkcnt, blkoff, L.nblk, hdr);
+    prof_mark(KK_SCAN, false, s);
+    prof_mark(KK_WRITE_IDX, true, s);
+    k_write_idx<<<L.nblk, kThreads, 0, s>>>(keep, cu, R, N, blkoff, targets, V,
+                                             reinterpret_cast<int32_t*>(ws + L.idx),
+                                             reinterpret_cast<int32_t*>(ws + L.tokr),
+                                             reinterpret_cast<int32_t*>(ws + L.ytgt),
+                                             reinterpret_cast<float*>(ws + L.zy), hdr);
+    prof_mark(KK_WRITE_IDX, false, s);
+  }
+  if (R > 0) {
+    prof_mark(KK_ROLLOUT_OFFSETS, true, s);
+    k_rollout_offsets<<<blocks_for(R, kThreads), kThreads, 0, s>>>(
+        cu, R, N, reinterpret_cast<const int32_t*>(ws + L.idx), hdr,
+        reinterpret_cast<int32_t*>(ws + L.rstart), reinterpret_cast<int32_t*>(ws + L.rnpol));
+    prof_mark(KK_ROLLOUT_OFFSETS, false, s);
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_advantage(int R, const float* rewards, const int32_t* gid, float adv_eps, int32_t* first,
+                            int32_t* gidx, int32_t* gsize, double* gmu, double* gsig, int32_t* geq,
+                            float* adv, WsHeader* hdr, hipStream_t s) {
+  if (R <= 0) return hipSuccess;
+  prof_mark(KK_GROUP_RANK, true, s);
+  k_group_first<<<blocks_for(R, kThreads), kThreads, 0, s>>>(gid, R, first);
+  k_group_rank<<<blocks_for(R, kThreads), kThreads, 0, s>>>(gid, R, first, gidx, hdr);
+  prof_mark(KK_GROUP_RANK, false, s);
+  prof_mark(KK_GROUP_STATS, true, s);
+  k_group_stats<<<blocks_for(R, kThreads / 64), kThreads, 0, s>>>(rewards, gidx, R, hdr, gsize, gmu, gsig,
+                                                                   geq);
+  prof_mark(KK_GROUP_STATS, false, s);
+  prof_mark(KK_ADVANTAGE, true, s);
+  k_advantage<<<blocks_for(R, kThreads), kThreads, 0, s>>>(rewards, gidx, R, gmu, gsig, geq, adv_eps, adv);
+  prof_mark(KK_ADVANTAGE, false, s);
+  return hipGetLastError();
+}
+
+}  // namespace rlk

@@ -1,0 +1,430 @@
+// Per-token kernels of the hot path: operand gathers/transposes, the merge of the online
+// log-softmax partials, the loss terms and their per-token backward scalars, the logits
+// gradient dz, the deterministic loss reduction and the zero fill of untrained rows.
+//
+// Notation (ClawGym II, Sec. 2.3): z = W h, lse = logsumexp(z), logp = z_y - lse,
+// H = -sum_j p_j log p_j, rho = exp(logp - old_logp), A = group advantage of the token's
+// rollout, s = min(rho A, clip(rho, 1-eps_lo, 1+eps_hi) A), loss L = sum_t w_t (s_t + c H_t)
+// with w_t = -1/(Q G_q n_r) for the per-rollout/per-group mean (masked GRPO objective,
+// Sec. 2.3.2 with the tree rule of Sec. 3.2.3) or -1/sum M for the token mean (Sec. 2.3.1).
+// Backward: dL/dlogp_t = g_t = w_t A rho_t [not clipped], dL/dH_t = e_t = w_t c, and
+//   dz_tj = g_t ([j = y_t] - p_tj) - e_t p_tj (z_tj - lse_t + H_t).
+#include "rlk_internal.h"
+
+namespace rlk {
+
+namespace {
+
+constexpr float kLog2e = 1.4426950408889634f;
+
+__device__ __forceinline__ float bf16_to_f(uint16_t b) { return __uint_as_float(((uint32_t)b) << 16); }
+__device__ __forceinline__ uint16_t f_to_bf16(float x) { return __builtin_bit_cast(uint16_t, (__bf16)x); }
+
+template <typename X>
+__device__ inline X wave_sum(X v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+
+// 16-byte vectors of 8 bf16 (stored as uint16_t bit patterns) or 4 fp32 elements.
+template <typename T>
+__device__ __forceinline__ float vget(const u32x4& v, int k) {
+  if constexpr (sizeof(T) == 2) {
+    const uint32_t w = v[k >> 1];
+    return bf16_to_f((uint16_t)((k & 1) ? (w >> 16) : (w & 0xffffu)));
+  } else {
+    return __uint_as_float(v[k]);
+  }
+}
+
+template <typename T>
+__device__ __forceinline__ T to_storage(float x) {
+  if constexpr (sizeof(T) == 2) return f_to_bf16(x);
+  else return x;
+}
+
+template <typename T>
+__device__ __forceinline__ u32x4 vpack(const T* e) {
+  u32x4 v;
+  if constexpr (sizeof(T) == 2) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) v[j] = (uint32_t)e[2 * j] | ((uint32_t)e[2 * j + 1] << 16);
+  } else {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) v[j] = __float_as_uint(e[j]);
+  }
+  return v;
+}
+
+// ---- W^T [d][Vp] (zero rows beyond V) for the dhidden GEMM, 64 x 64 tiles through LDS.
+template <typename T>
+__global__ void __launch_bounds__(256) k_transpose_w(const T* W, T* WT, int V, int64_t Vp, int d) {
+  __shared__ T tile[64][65];
+  const int64_t v0 = (int64_t)blockIdx.x * 64;
+  const int j0 = blockIdx.y * 64;
+  for (int e = threadIdx.x; e < 64 * 64; e += 256) {
+    const int r = e >> 6, c = e & 63;
+    T val = 0;
+    if (v0 + r < V && j0 + c < d) val = W[(v0 + r) * d + j0 + c];
+    tile[r][c] = val;
+  }
+  __syncthreads();
+  for (int e = threadIdx.x; e < 64 * 64; e += 256) {
+    const int r = e >> 6, c = e & 63;   // r: feature, c: vocabulary
+    if (j0 + r < d && v0 + c < Vp) WT[(int64_t)(j0 + r) * Vp + v0 + c] = tile[c][r];
+  }
+}
+
+// ---- Hc[t][:] = hidden[idx[c0 + t]][:] and HT[j][t] (zero columns t >= rows, up to the K pad).
+template <typename T>
+__global__ void __launch_bounds__(256)
+k_gather(const T* hidden, int d, const int32_t* idx, const WsHeader* hdr, int64_t c0, int64_t Mc, T* hc, T* ht,
+         int want_ht) {
+  constexpr int EPC = 16 / sizeof(T);     // elements per 16-byte chunk
+  constexpr int CPR = 64 / EPC;           // chunks per 64-feature row slice
+  __shared__ __attribute__((aligned(16))) T tile[64][64 + EPC];
+  int64_t rc = (int64_t)hdr->n_eff - c0;
+  rc = rc < 0 ? 0 : (rc > Mc ? Mc : rc);
+  const int64_t rpad = (rc + kKAlign - 1) / kKAlign * kKAlign;
+  const int64_t t0 = (int64_t)blockIdx.x * 64;
+  const int j0 = blockIdx.y * 64;
+  if (t0 >= rpad) return;
+  for (int c = threadIdx.x; c < 64 * CPR; c += 256) {
+    const int tl = c / CPR, ch = c % CPR;
+    const int64_t t = t0 + tl;
+    const int j = j0 + ch * EPC;
+    u32x4 v = u32x4{0, 0, 0, 0};
+    if (t < rc && j < d) {
+      const int64_t row = idx[c0 + t];
+      v = *reinterpret_cast<const u32x4*>(hidden + row * d + j);
+      *reinterpret_cast<u32x4*>(hc + t * d + j) = v;
+    }
+    *reinterpret_cast<u32x4*>(&tile[tl][ch * EPC]) = v;
+  }
+  if (!want_ht) return;
+  __syncthreads();
+  for (int c = threadIdx.x; c < 64 * CPR; c += 256) {
+    const int jl = c / CPR, ch = c % CPR;   // feature row of HT, chunk of 8/4 tokens
+    const int j = j0 + jl;
+    if (j >= d) continue;
+    T vals[EPC];
+#pragma unroll
+    for (int i = 0; i < EPC; ++i) vals[i] = tile[ch * EPC + i][jl];
+    *reinterpret_cast<u32x4*>(ht + (int64_t)j * Mc + t0 + ch * EPC) = vpack<T>(vals);
+  }
+}
+
+// ---- merge of the per-vocabulary-tile partials (m, s, u) into lse, logp, H; loss scalars.
+__global__ void __launch_bounds__(256) k_combine(TokenParams p) {
+  int64_t rc = (int64_t)p.hdr->n_eff - p.c0;
+  rc = rc < 0 ? 0 : (rc > p.Mc ? p.Mc : rc);
+  const int64_t tl = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (tl >= rc) return;
+  const int64_t i = p.c0 + tl;
+  float M = -INFINITY;
+  for (int k = 0; k < p.nvt; ++k) M = fmaxf(M, p.pm[(int64_t)k * p.Mc + tl]);
+  double S = 0.0;
+  for (int k = 0; k < p.nvt; ++k) {
+    const int64_t o = (int64_t)k * p.Mc + tl;
+    S += (double)p.ps[o] * (double)__builtin_amdgcn_exp2f((p.pm[o] - M) * kLog2e);
+  }
+  const double lse = (double)M + log(S);
+  // sum_j p_j (z_j - lse) = sum_k e^{m_k - lse} (u_k + (m_k - lse) s_k)
+  double E = 0.0;
+  for (int k = 0; k < p.nvt; ++k) {
+    const int64_t o = (int64_t)k * p.Mc + tl;
+    const double dm = (double)p.pm[o] - lse;
+    E += exp(dm) * ((double)p.pu[o] + dm * (double)p.ps[o]);
+  }
+  const float lsef = (float)lse;
+  const float H = (float)(-E);
+  const float logp = (float)((double)p.zy[i] - lse);
+  p.lse[i] = lsef;
+  p.logp[i] = logp;
+  p.ent[i] = H;
+  const int64_t row = p.idx[i];
+  if (p.logp_out) p.logp_out[row] = logp;
+  if (p.ent_out) p.ent_out[row] = H;
+  if (p.lse_out) p.lse_out[row] = lsef;
+  if (p.with_grad) {
+    const int r = p.tokr[i];
+    const float A = p.adv[r];
+    const float rho = expf(logp - p.old_logp[row]);
+    double w;
+    if (p.agg == RLK_AGG_SEQ_MEAN_TOKEN_MEAN) {
+      const double Qn = p.norm_override > 0 ? p.norm_override : (double)p.hdr->n_groups;
+      w = -1.0 / (Qn * (double)p.gsize[p.gidx[r]] * (double)p.rnpol[r]);
+    } else {
+      const double Mn = p.norm_override > 0 ? p.norm_override : (double)p.hdr->n_eff;
+      w = -1.0 / Mn;
+    }
+    const bool clipped = (A > 0.0f && rho > 1.0f + p.eps_high) || (A < 0.0f && rho < 1.0f - p.eps_low);
+    p.gt[i] = clipped ? 0.0f : (float)(w * (double)A * (double)rho);
+    p.et[i] = (float)(w * (double)p.ent_coef);
+  }
+}
+
+// ---- dz for a chunk: q holds exp(z - m_tile) per (token, vocabulary); rewritten in place with
+// dz and also written transposed for the dW GEMM.  Tile: 64 tokens x 256 vocabulary entries
+// (one forward vocabulary tile, so one m_tile per token).
+template <typename T, bool ENT>
+__global__ void __launch_bounds__(256) k_dz(DzParams p) {
+  constexpr int EPC = 16 / sizeof(T);
+  constexpr int CPR = kVocabTile / EPC;          // chunks per token row of the tile
+  constexpr int PAD = EPC;
+  __shared__ __attribute__((aligned(16))) T sT[kVocabTile][64 + PAD];
+  int64_t rc = (int64_t)p.hdr->n_eff - p.c0;
+  rc = rc < 0 ? 0 : (rc > p.Mc ? p.Mc : rc);
+  const int64_t rpad = (rc + kKAlign - 1) / kKAlign * kKAlign;
+  const int vt = blockIdx.x;
+  const int64_t v0 = (int64_t)vt * kVocabTile;
+  const int64_t t0 = (int64_t)blockIdx.y * 64;
+  if (t0 >= rpad) return;
+  T* q = reinterpret_cast<T*>(p.q);
+  for (int c = threadIdx.x; c < 64 * CPR; c += 256) {
+    const int tl = c / CPR, ch = c % CPR;
+    const int64_t t = t0 + tl;
+    if (t < rc) {
+      const int64_t i = p.c0 + t;
+      const float lse = p.lse[i], logp = p.logp[i], H = p.ent[i], g = p.gt[i], e = p.et[i];
+      const int y = p.ytgt[i];
+      const float mk = p.pm[(int64_t)vt * p.Mc + t];
+      const float sc = __builtin_amdgcn_exp2f((mk - lse) * kLog2e);
+      const float base = mk - lse + H;    // z - lse + H = log q + base
+      T* qp = q + t * p.Vp + v0 + ch * EPC;
+      const u32x4 raw = *reinterpret_cast<const u32x4*>(qp);
+      T o[EPC];
+#pragma unroll
+      for (int k = 0; k < EPC; ++k) {
+        const float qv = vget<T>(raw, k);
+        const int64_t v = v0 + ch * EPC + k;
+        float dz;
+        if (v == y) {
+          // the target entry uses the exact fp32 log-prob: 1 - p_y = -expm1(logp)
+          dz = g * (-expm1f(logp));
+          if (ENT) dz -= e * expf(logp) * (logp + H);
+        } else {
+          const float pr = qv * sc;
+          float coef = g;
+          if (ENT) coef += (qv > 0.0f) ? e * (__logf(qv) + base) : 0.0f;
+          dz = -pr * coef;
+        }
+        o[k] = to_storage<T>(dz);
+      }
+      *reinterpret_cast<u32x4*>(qp) = vpack<T>(o);
+#pragma unroll
+      for (int k = 0; k < EPC; ++k) sT[ch * EPC + k][tl] = o[k];
+    } else {
+#pragma unroll
+      for (int k = 0; k < EPC; ++k) sT[ch * EPC + k][tl] = (T)0;
+    }
+  }
+  __syncthreads();
+  T* dzt = reinterpret_cast<T*>(p.dzt);
+  constexpr int TCH = 64 / EPC;   // 16-byte chunks per transposed row (64 tokens)
+  for (int c = threadIdx.x; c < kVocabTile * TCH; c += 256) {
+    const int vl = c / TCH, ch = c % TCH;
+    *reinterpret_cast<u32x4*>(dzt + (v0 + vl) * p.Mc + t0 + ch * EPC) =
+        *reinterpret_cast<const u32x4*>(&sT[vl][ch * EPC]);
+  }
+}
+
+// ---- deterministic loss reduction: per-rollout fp64 sums, then one block over rollouts.
+__global__ void __launch_bounds__(256) k_loss_rollout(LossParams p) {
+  __shared__ double sh[4][4];
+  const int r = blockIdx.x;
+  const int n = p.rnpol[r];
+  const int s0 = p.rstart[r];
+  const float A = p.adv[r];
+  double ss = 0.0, sH = 0.0, sR = 0.0, sC = 0.0;
+  if (p.gidx[r] >= 0) {
+    for (int k = threadIdx.x; k < n; k += 256) {
+      const int i = s0 + k;
+      const float logp = p.logp[i];
+      const float rho = expf(logp - p.old_logp[p.idx[i]]);
+      const float lo = 1.0f - p.eps_low, hi = 1.0f + p.eps_high;
+      const float cr = fminf(fmaxf(rho, lo), hi);
+      const float s = fminf(rho * A, cr * A);
+      const bool clipped = (A > 0.0f && rho > hi) || (A < 0.0f && rho < lo);
+      ss += (double)s;
+      sH += (double)p.ent[i];
+      sR += (double)rho;
+      sC += clipped ? 1.0 : 0.0;
+    }
+  }
+  ss = wave_sum(ss);
+  sH = wave_sum(sH);
+  sR = wave_sum(sR);
+  sC = wave_sum(sC);
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  if (lane == 0) {
+    sh[w][0] = ss;
+    sh[w][1] = sH;
+    sh[w][2] = sR;
+    sh[w][3] = sC;
+  }
+  __syncthreads();
+  if (threadIdx.x < 4) {
+    double t = 0.0;
+    for (int k = 0; k < 4; ++k) t += sh[k][threadIdx.x];
+    p.rsum[(int64_t)r * 4 + threadIdx.x] = t;
+  }
+}
+
+__global__ void __launch_bounds__(1024) k_loss_final(LossParams p) {
+  __shared__ double sh[16][5];
+  double J = 0.0, Jpg = 0.0, tH = 0.0, tR = 0.0, tC = 0.0;
+  const double c = (double)p.ent_coef;
+  for (int r = threadIdx.x; r < p.R; r += 1024) {
+    const int q = p.gidx[r];
+    const int n = p.rnpol[r];
+    if (q < 0 || n == 0) continue;
+    const double* rs = p.rsum + (int64_t)r * 4;
+    if (p.agg == RLK_AGG_SEQ_MEAN_TOKEN_MEAN) {
+      const double denom = (double)n * (double)p.gsize[q];
+      J += (rs[0] + c * rs[1]) / denom;
+      Jpg += rs[0] / denom;
+    } else {
+      J += rs[0] + c * rs[1];
+      Jpg += rs[0];
+    }
+    tH += rs[1];
+    tR += rs[2];
+    tC += rs[3];
+  }
+  J = wave_sum(J);
+  Jpg = wave_sum(Jpg);
+  tH = wave_sum(tH);
+  tR = wave_sum(tR);
+  tC = wave_sum(tC);
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  if (lane == 0) {
+    sh[w][0] = J;
+    sh[w][1] = Jpg;
+    sh[w][2] = tH;
+    sh[w][3] = tR;
+    sh[w][4] = tC;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    double a[5] = {0, 0, 0, 0, 0};
+    for (int k = 0; k < 16; ++k)
+      for (int f = 0; f < 5; ++f) a[f] += sh[k][f];
+    const int n_eff = p.hdr->n_eff;
+    const int Q = p.hdr->n_groups;
+    double norm;
+    if (p.agg == RLK_AGG_SEQ_MEAN_TOKEN_MEAN) norm = p.norm_override > 0 ? p.norm_override : (double)Q;
+    else norm = p.norm_override > 0 ? p.norm_override : (double)n_eff;
+    const bool empty = n_eff == 0 || Q == 0;
+    const float loss = empty ? 0.0f : (float)(-a[0] / norm);
+    const float pg = empty ? 0.0f : (float)(-a[1] / norm);
+    if (p.loss) p.loss[0] = loss;
+    if (p.stats) {
+      rlk_pg_stats_t st;
+      st.loss = loss;
+      st.pg_loss = pg;
+      st.entropy_mean = n_eff ? (float)(a[2] / n_eff) : 0.0f;
+      st.ratio_mean = n_eff ? (float)(a[3] / n_eff) : 0.0f;
+      st.clip_frac = n_eff ? (float)(a[4] / n_eff) : 0.0f;
+      st.n_groups = Q;
+      st.n_valid_rollouts = p.hdr->n_valid;
+      st.n_policy_tokens = n_eff;
+      *p.stats = st;
+    }
+  }
+}
+
+// ---- rows that are not trained: dhidden row = 0 and the scattered per-token outputs = 0.
+template <typename T>
+__global__ void __launch_bounds__(256)
+k_zero_fill(const uint8_t* keep, int64_t N, int d, T* dh, float* o1, float* o2, float* o3) {
+  const int64_t t = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (t >= N || keep[t]) return;
+  const int lane = threadIdx.x & 63;
+  if (lane == 0) {
+    if (o1) o1[t] = 0.0f;
+    if (o2) o2[t] = 0.0f;
+    if (o3) o3[t] = 0.0f;
+  }
+  if (!dh) return;
+  constexpr int EPC = 16 / sizeof(T);
+  const int nch = d / EPC;
+  u32x4* row = reinterpret_cast<u32x4*>(dh + t * d);
+  for (int c = lane; c < nch; c += 64) row[c] = u32x4{0, 0, 0, 0};
+}
+
+}  // namespace
+
+hipError_t launch_transpose_w(int dtype, const void* W, void* WT, int V, int64_t Vp, int d, hipStream_t s) {
+  dim3 grid((unsigned)(Vp / 64), (unsigned)((d + 63) / 64));
+  prof_mark(KK_TRANSPOSE_W, true, s);
+  if (dtype == RLK_DTYPE_BF16)
+    k_transpose_w<uint16_t><<<grid, 256, 0, s>>>((const uint16_t*)W, (uint16_t*)WT, V, Vp, d);
+  else
+    k_transpose_w<float><<<grid, 256, 0, s>>>((const float*)W, (float*)WT, V, Vp, d);
+  prof_mark(KK_TRANSPOSE_W, false, s);
+  return hipGetLastError();
+}
+
+hipError_t launch_gather(int dtype, const void* hidden, int d, const int32_t* idx, const WsHeader* hdr, int64_t c0,
+                         int64_t Mc, void* hc, void* ht, bool want_ht, hipStream_t s) {
+  dim3 grid((unsigned)(Mc / 64), (unsigned)((d + 63) / 64));
+  prof_mark(KK_GATHER, true, s);
+  if (dtype == RLK_DTYPE_BF16)
+    k_gather<uint16_t><<<grid, 256, 0, s>>>((const uint16_t*)hidden, d, idx, hdr, c0, Mc, (uint16_t*)hc,
+                                            (uint16_t*)ht, want_ht ? 1 : 0);
+  else
+    k_gather<float><<<grid, 256, 0, s>>>((const float*)hidden, d, idx, hdr, c0, Mc, (float*)hc, (float*)ht,
+                                         want_ht ? 1 : 0);
+  prof_mark(KK_GATHER, false, s);
+  return hipGetLastError();
+}
+
+hipError_t launch_combine(const TokenParams& p, hipStream_t s) {
+  prof_mark(KK_COMBINE, true, s);
+  k_combine<<<(unsigned)((p.Mc + 255) / 256), 256, 0, s>>>(p);
+  prof_mark(KK_COMBINE, false, s);
+  return hipGetLastError();
+}
+
+hipError_t launch_dz(int dtype, const DzParams& p, hipStream_t s) {
+  dim3 grid((unsigned)(p.Vp / kVocabTile), (unsigned)(p.Mc / 64));
+  prof_mark(KK_DZ, true, s);
+  if (dtype == RLK_DTYPE_BF16) {
+    if (p.has_ent) k_dz<uint16_t, true><<<grid, 256, 0, s>>>(p);
+    else k_dz<uint16_t, false><<<grid, 256, 0, s>>>(p);
+  } else {
+    if (p.has_ent) k_dz<float, true><<<grid, 256, 0, s>>>(p);
+    else k_dz<float, false><<<grid, 256, 0, s>>>(p);
+  }
+  prof_mark(KK_DZ, false, s);
+  return hipGetLastError();
+}
+
+hipError_t launch_loss(const LossParams& p, hipStream_t s, int) {
+  if (p.R > 0) {
+    prof_mark(KK_LOSS_ROLLOUT, true, s);
+    k_loss_rollout<<<p.R, 256, 0, s>>>(p);
+    prof_mark(KK_LOSS_ROLLOUT, false, s);
+  }
+  prof_mark(KK_LOSS_FINAL, true, s);
+  k_loss_final<<<1, 1024, 0, s>>>(p);
+  prof_mark(KK_LOSS_FINAL, false, s);
+  return hipGetLastError();
+}
+
+hipError_t launch_zero_fill(int dtype, const uint8_t* keep, int64_t N, int d, void* dh, float* o1, float* o2,
+                            float* o3, hipStream_t s) {
+  if (N <= 0) return hipSuccess;
+  prof_mark(KK_ZERO_FILL, true, s);
+  const unsigned blocks = (unsigned)((N + 3) / 4);
+  if (dtype == RLK_DTYPE_BF16)
+    k_zero_fill<uint16_t><<<blocks, 256, 0, s>>>(keep, N, d, (uint16_t*)dh, o1, o2, o3);
+  else
+    k_zero_fill<float><<<blocks, 256, 0, s>>>(keep, N, d, (float*)dh, o1, o2, o3);
+  prof_mark(KK_ZERO_FILL, false, s);
+  return hipGetLastError();
+}
+
+}  // namespace rlk

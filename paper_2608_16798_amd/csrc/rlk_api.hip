@@ -1,0 +1,614 @@
+// C-ABI entry points of librlk: argument validation, workspace layout, the chunk loop and
+// the launch sequence of the hot path.  No device memory is allocated here; every buffer
+// comes from the caller.
+#include <math.h>
+#include <stdarg.h>
+#include <stdio.h>
+#include <stdlib.h>
+#include <string.h>
+
+#include <mutex>
+#include <string>
+#include <vector>
+
+#include "rlk_internal.h"
+
+namespace rlk {
+
+namespace {
+
+thread_local std::string g_last_error;
+
+rlk_status_t fail(rlk_status_t code, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
+rlk_status_t fail(rlk_status_t code, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return code;
+}
+
+rlk_status_t hip_fail(hipError_t e, const char* what) {
+  return fail(RLK_EHIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+inline int64_t roundup(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
+
+struct Alloc {
+  size_t off = 0;
+  size_t take(size_t bytes) {
+    size_t o = off;
+    off = align256(off + bytes);
+    return o;
+  }
+};
+
+bool debug_sync() {
+  static int v = -1;
+  if (v < 0) {
+    const char* e = getenv("RLK_DEBUG_SYNC");
+    v = (e && e[0] && e[0] != '0') ? 1 : 0;
+  }
+  return v == 1;
+}
+
+rlk_status_t check_batch(const rlk_batch_t* b) {
+  if (!b) return fail(RLK_EINVAL, "batch descriptor is NULL");
+  if (b->dtype != RLK_DTYPE_F32 && b->dtype != RLK_DTYPE_BF16) return fail(RLK_EDTYPE, "unknown dtype %d", b->dtype);
+  if (b->N < 0 || b->R < 0) return fail(RLK_ESHAPE, "negative N (%lld) or R (%d)", (long long)b->N, b->R);
+  if (b->N >= ((int64_t)1 << 31)) return fail(RLK_ESHAPE, "N = %lld exceeds the int32 token index", (long long)b->N);
+  if (b->R == 0 && b->N != 0) return fail(RLK_ESHAPE, "R = 0 with N = %lld tokens", (long long)b->N);
+  if (b->R > kMaxRollouts) return fail(RLK_ESHAPE, "R = %d exceeds the supported %d rollouts", b->R, kMaxRollouts);
+  if (b->d < 8 || b->d % 8 != 0) return fail(RLK_ESHAPE, "d = %d must be a positive multiple of 8", b->d);
+  if (b->V < 1) return fail(RLK_ESHAPE, "V = %d must be positive", b->V);
+  if (b->R > 0 && !b->cu_seqlens) return fail(RLK_EINVAL, "cu_seqlens is NULL");
+  return RLK_OK;
+}
+
+rlk_status_t layout(const rlk_batch_t* b, bool bwd, int64_t chunk_rows, WsLayout& L) {
+  const int64_t esz = b->dtype == RLK_DTYPE_BF16 ? 2 : 4;
+  const int64_t N = b->N, R = b->R, d = b->d, V = b->V;
+  L.Vp = roundup(V, kVocabTile);
+  L.nvt = (int32_t)(L.Vp / kVocabTile);
+  L.nblk = (int32_t)((N + kScanTile - 1) / kScanTile);
+  if (L.nblk < 1) L.nblk = 1;
+  if (chunk_rows < 0 || chunk_rows % kChunkAlign != 0)
+    return fail(RLK_ESHAPE, "chunk_rows = %lld must be a non-negative multiple of %d", (long long)chunk_rows,
+                kChunkAlign);
+  int64_t Mc = chunk_rows;
+  if (Mc == 0) {
+    int64_t per_row = (int64_t)L.nvt * 12 + d * esz;
+    if (bwd) per_row += d * esz + 2 * L.Vp * esz;
+    const int64_t budget = bwd ? ((int64_t)24 << 30) : ((int64_t)4 << 30);
+    Mc = budget / per_row / kChunkAlign * kChunkAlign;
+    if (Mc > 65536) Mc = 65536;
+    if (Mc < kChunkAlign) Mc = kChunkAlign;
+    const int64_t cap = roundup(N > 0 ? N : 1, kChunkAlign);
+    if (Mc > cap) Mc = cap;
+  }
+  L.Mc = Mc;
+  L.nchunks = (int32_t)((N + Mc - 1) / Mc);
+  if (bwd && L.nchunks < 1) L.nchunks = 1;
+
+  Alloc a;
+  L.hdr = a.take(sizeof(WsHeader));
+  L.keep = a.take((size_t)N);
+  L.blkcnt = a.take((size_t)L.nblk * 4);
+  L.blkoff = a.take((size_t)L.nblk * 4);
+  L.idx = a.take((size_t)N * 4);
+  L.tokr = a.take((size_t)N * 4);
+  L.ytgt = a.take((size_t)N * 4);
+  L.zy = a.take((size_t)N * 4);
+  L.lse = a.take((size_t)N * 4);
+  L.logp = a.take((size_t)N * 4);
+  L.ent = a.take((size_t)N * 4);
+  L.gt = a.take((size_t)N * 4);
+  L.et = a.take((size_t)N * 4);
+  L.rstart = a.take((size_t)R * 4);
+  L.rnpol = a.take((size_t)R * 4);
+  L.first = a.take((size_t)R * 4);
+  L.gidx = a.take((size_t)R * 4);
+  L.gsize = a.take((size_t)R * 4);
+  L.gmu = a.take((size_t)R * 8);
+  L.gsig = a.take((size_t)R * 8);
+  L.geq = a.take((size_t)R * 4);
+  L.adv = a.take((size_t)R * 4);
+  L.rsum = a.take((size_t)R * 32);
+  L.pm = a.take((size_t)L.nvt * Mc * 4);
+  L.ps = a.take((size_t)L.nvt * Mc * 4);
+  L.pu = a.take((size_t)L.nvt * Mc * 4);
+  L.hc = a.take((size_t)(Mc * d * esz));
+  if (bwd) {
+    L.ht = a.take((size_t)(d * Mc * esz));
+    L.q = a.take((size_t)(Mc * L.Vp * esz));
+    L.dzt = a.take((size_t)(L.Vp * Mc * esz));
+    L.wt = a.take((size_t)(d * L.Vp * esz));
+  }
+  L.total = a.off;
+  return RLK_OK;
+}
+
+size_t advantage_ws_bytes(int32_t R) {
+  Alloc a;
+  a.take(sizeof(WsHeader));
+  a.take((size_t)R * 4);  // first
+  a.take((size_t)R * 4);  // gidx
+  a.take((size_t)R * 4);  // gsize
+  a.take((size_t)R * 8);  // mu
+  a.take((size_t)R * 8);  // sigma
+  a.take((size_t)R * 4);  // all-equal flags
+  return a.off;
+}
+
+rlk_status_t check_ws(const void* ws, size_t have, size_t need) {
+  if (!ws) return fail(RLK_EWORKSPACE, "workspace is NULL");
+  if (reinterpret_cast<uintptr_t>(ws) % 256 != 0) return fail(RLK_EWORKSPACE, "workspace must be 256-byte aligned");
+  if (have < need)
+    return fail(RLK_EWORKSPACE, "workspace has %zu bytes, %zu needed", have, need);
+  return RLK_OK;
+}
+
+rlk_status_t finish(hipError_t e, const char* what, const void* ws, hipStream_t s) {
+  if (e != hipSuccess) return hip_fail(e, what);
+  if (debug_sync()) {
+    hipError_t e2 = hipStreamSynchronize(s);
+    if (e2 != hipSuccess) return hip_fail(e2, "hipStreamSynchronize");
+    int32_t st = 0;
+    e2 = hipMemcpy(&st, ws, sizeof(int32_t), hipMemcpyDeviceToHost);
+    if (e2 != hipSuccess) return hip_fail(e2, "hipMemcpy(status)");
+    if (st != 0) return fail(RLK_EDATA, "device data error flags 0x%x", st);
+  }
+  return RLK_OK;
+}
+
+#define RLK_TRY(expr, what)                      \
+  do {                                           \
+    hipError_t _e = (expr);                      \
+    if (_e != hipSuccess) return hip_fail(_e, what); \
+  } while (0)
+
+// ---------------------------------------------------------------- profiling
+struct ProfRec {
+  int kind;
+  hipEvent_t a, b;
+};
+struct Prof {
+  std::mutex mu;
+  bool on = false;
+  std::vector<ProfRec> recs;
+  hipEvent_t open = nullptr;
+  int open_kind = -1;
+};
+Prof& prof() {
+  static Prof p;
+  return p;
+}
+
+const char* kKindNames[KK_COUNT_KINDS] = {
+    "begin",        "compact_count", "compact_scan",  "compact_write", "rollout_offsets", "group_rank",
+    "group_stats",  "advantage",     "transpose_w",   "gather",        "fwd_lse_gemm",    "lse_combine",
+    "dz",           "dh_gemm",       "dw_gemm",       "loss_rollout",  "loss_final",      "zero_fill"};
+
+}  // namespace
+
+void prof_mark(int kind, bool begin, hipStream_t s) {
+  Prof& P = prof();
+  if (!P.on) return;
+  std::lock_guard<std::mutex> lk(P.mu);
+  hipEvent_t ev;
+  if (hipEventCreate(&ev) != hipSuccess) return;
+  (void)hipEventRecord(ev, s);
+  if (begin) {
+    P.open = ev;
+    P.open_kind = kind;
+  } else if (P.open && P.open_kind == kind) {
+    P.recs.push_back({kind, P.open, ev});
+    P.open = nullptr;
+    P.open_kind = -1;
+  } else {
+    (void)hipEventDestroy(ev);
+  }
+}
+
+}  // namespace rlk
+
+using namespace rlk;
+
+extern "C" {
+
+rlk_status_t rlk_workspace_size(const rlk_batch_t* b, const rlk_pg_params_t* p, size_t* bytes) {
+  if (!bytes) return fail(RLK_EINVAL, "bytes is NULL");
+  rlk_status_t st = check_batch(b);
+  if (st) return st;
+  WsLayout L;
+  st = layout(b, p != nullptr, p ? p->chunk_rows : 0, L);
+  if (st) return st;
+  *bytes = L.total;
+  return RLK_OK;
+}
+
+rlk_status_t rlk_advantage_workspace_size(int32_t R, size_t* bytes) {
+  if (!bytes) return fail(RLK_EINVAL, "bytes is NULL");
+  if (R < 0 || R > kMaxRollouts) return fail(RLK_ESHAPE, "R = %d outside [0, %d]", R, kMaxRollouts);
+  *bytes = advantage_ws_bytes(R);
+  return RLK_OK;
+}
+
+rlk_status_t rlk_logprob_fwd(const rlk_batch_t* b, const void* hidden, const void* W, const int32_t* targets,
+                             const uint8_t* mask, float* logp, float* entropy, float* lse, void* ws,
+                             size_t ws_bytes, void* stream) {
+  rlk_status_t st = check_batch(b);
+  if (st) return st;
+  if (b->N > 0 && (!hidden || !targets || !logp)) return fail(RLK_EINVAL, "hidden, targets or logp is NULL");
+  if (!W) return fail(RLK_EINVAL, "W is NULL");
+  WsLayout L;
+  st = layout(b, false, 0, L);
+  if (st) return st;
+  st = check_ws(ws, ws_bytes, L.total);
+  if (st) return st;
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  char* w = static_cast<char*>(ws);
+  WsHeader* hdr = reinterpret_cast<WsHeader*>(w + L.hdr);
+  const int64_t N = b->N;
+
+  RLK_TRY(launch_begin(reinterpret_cast<int32_t*>(hdr), b->cu_seqlens, b->R, N, s), "begin");
+  if (N == 0) return finish(hipSuccess, "", ws, s);
+  RLK_TRY(launch_compact(mask, b->cu_seqlens, nullptr, b->R, N, targets, b->V, w, L, s), "compact");
+  for (int c = 0; c < L.nchunks; ++c) {
+    const int64_t c0 = (int64_t)c * L.Mc;
+    RLK_TRY(launch_gather(b->dtype, hidden, b->d, reinterpret_cast<const int32_t*>(w + L.idx), hdr, c0, L.Mc,
+                          w + L.hc, nullptr, false, s),
+            "gather");
+    GemmArgs g = {};
+    g.A = W;
+    g.B = w + L.hc;
+    g.lda = b->d;
+    g.ldb = b->d;
+    g.M = b->V;
+    g.N = (int)L.Mc;
+    g.K = b->d;
+    g.hdr = hdr;
+    g.c0 = c0;
+    g.Mc = L.Mc;
+    g.ytgt = reinterpret_cast<const int32_t*>(w + L.ytgt);
+    g.zy = reinterpret_cast<float*>(w + L.zy);
+    g.pm = reinterpret_cast<float*>(w + L.pm);
+    g.ps = reinterpret_cast<float*>(w + L.ps);
+    g.pu = reinterpret_cast<float*>(w + L.pu);
+    g.V = b->V;
+    RLK_TRY(launch_fwd_gemm(b->dtype, g, false, s), "fwd_gemm");
+    TokenParams tp = {};
+    tp.hdr = hdr;
+    tp.c0 = c0;
+    tp.Mc = L.Mc;
+    tp.nvt = L.nvt;
+    tp.pm = g.pm;
+    tp.ps = g.ps;
+    tp.pu = g.pu;
+    tp.zy = g.zy;
+    tp.idx = reinterpret_cast<const int32_t*>(w + L.idx);
+    tp.tokr = reinterpret_cast<const int32_t*>(w + L.tokr);
+    tp.ytgt = g.ytgt;
+    tp.lse = reinterpret_cast<float*>(w + L.lse);
+    tp.logp = reinterpret_cast<float*>(w + L.logp);
+    tp.ent = reinterpret_cast<float*>(w + L.ent);
+    tp.gt = reinterpret_cast<float*>(w + L.gt);
+    tp.et = reinterpret_cast<float*>(w + L.et);
+    tp.logp_out = logp;
+    tp.ent_out = entropy;
+    tp.lse_out = lse;
+    tp.with_grad = 0;
+    RLK_TRY(launch_combine(tp, s), "combine");
+  }
+  RLK_TRY(launch_zero_fill(b->dtype, reinterpret_cast<const uint8_t*>(w + L.keep), N, b->d, nullptr, logp, entropy,
+                           lse, s),
+          "zero_fill");
+  return finish(hipSuccess, "", ws, s);
+}
+
+rlk_status_t rlk_compact(const rlk_batch_t* b, const uint8_t* mask, const int32_t* group_ids,
+                         const int32_t* targets, int32_t* idx, int32_t* tok_rollout, int32_t* n_pol, int32_t* n_eff,
+                         void* ws, size_t ws_bytes, void* stream) {
+  rlk_status_t st = check_batch(b);
+  if (st) return st;
+  if (!n_eff || (b->N > 0 && (!idx || !tok_rollout)) || (b->R > 0 && !n_pol))
+    return fail(RLK_EINVAL, "idx, tok_rollout, n_pol or n_eff is NULL");
+  WsLayout L;
+  st = layout(b, false, 0, L);
+  if (st) return st;
+  st = check_ws(ws, ws_bytes, L.total);
+  if (st) return st;
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  char* w = static_cast<char*>(ws);
+  WsHeader* hdr = reinterpret_cast<WsHeader*>(w + L.hdr);
+  RLK_TRY(launch_begin(reinterpret_cast<int32_t*>(hdr), b->cu_seqlens, b->R, b->N, s), "begin");
+  RLK_TRY(launch_compact(mask, b->cu_seqlens, group_ids, b->R, b->N, targets, b->V, w, L, s), "compact");
+  if (b->N > 0) {
+    RLK_TRY(hipMemcpyAsync(idx, w + L.idx, (size_t)b->N * 4, hipMemcpyDeviceToDevice, s), "copy idx");
+    RLK_TRY(hipMemcpyAsync(tok_rollout, w + L.tokr, (size_t)b->N * 4, hipMemcpyDeviceToDevice, s), "copy tok_rollout");
+  }
+  if (b->R > 0)
+    RLK_TRY(hipMemcpyAsync(n_pol, w + L.rnpol, (size_t)b->R * 4, hipMemcpyDeviceToDevice, s), "copy n_pol");
+  RLK_TRY(hipMemcpyAsync(n_eff, &hdr->n_eff, 4, hipMemcpyDeviceToDevice, s), "copy n_eff");
+  return finish(hipSuccess, "", ws, s);
+}
+
+rlk_status_t rlk_group_advantage(int32_t R, const float* rewards, const int32_t* group_ids, float adv_eps,
+                                 float* adv, int32_t* group_index, int32_t* n_groups, void* ws, size_t ws_bytes,
+                                 void* stream) {
+  if (R < 0 || R > kMaxRollouts) return fail(RLK_ESHAPE, "R = %d outside [0, %d]", R, kMaxRollouts);
+  if (R > 0 && (!rewards || !group_ids || !adv)) return fail(RLK_EINVAL, "rewards, group_ids or adv is NULL");
+  if (!(adv_eps >= 0.0f) || !isfinite(adv_eps)) return fail(RLK_EINVAL, "adv_eps must be finite and >= 0");
+  rlk_status_t st = check_ws(ws, ws_bytes, advantage_ws_bytes(R));
+  if (st) return st;
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  Alloc a;
+  char* w = static_cast<char*>(ws);
+  WsHeader* hdr = reinterpret_cast<WsHeader*>(w + a.take(sizeof(WsHeader)));
+  int32_t* first = reinterpret_cast<int32_t*>(w + a.take((size_t)R * 4));
+  int32_t* gidx_ws = reinterpret_cast<int32_t*>(w + a.take((size_t)R * 4));
+  int32_t* gsize = reinterpret_cast<int32_t*>(w + a.take((size_t)R * 4));
+  double* gmu = reinterpret_cast<double*>(w + a.take((size_t)R * 8));
+  double* gsig = reinterpret_cast<double*>(w + a.take((size_t)R * 8));
+  int32_t* geq = reinterpret_cast<int32_t*>(w + a.take((size_t)R * 4));
+  int32_t* gidx = group_index ? group_index : gidx_ws;
+  RLK_TRY(launch_begin(reinterpret_cast<int32_t*>(hdr), nullptr, 0, 0, s), "begin");
+  RLK_TRY(launch_advantage(R, rewards, group_ids, adv_eps, first, gidx, gsize, gmu, gsig, geq, adv, hdr, s),
+          "advantage");
+  if (n_groups)
+    RLK_TRY(hipMemcpyAsync(n_groups, &hdr->n_groups, sizeof(int32_t), hipMemcpyDeviceToDevice, s), "copy n_groups");
+  return finish(hipSuccess, "", ws, s);
+}
+
+rlk_status_t rlk_pg_loss_fwd_bwd(const rlk_batch_t* b, const void* hidden, const void* W, const int32_t* targets,
+                                 const uint8_t* mask, const float* old_logp, const float* rewards,
+                                 const int32_t* group_ids, const rlk_pg_params_t* p, float* loss, void* dhidden,
+                                 float* dW, float* logp_out, float* entropy_out, rlk_pg_stats_t* stats, void* ws,
+                                 size_t ws_bytes, void* stream) {
+  rlk_status_t st = check_batch(b);
+  if (st) return st;
+  if (!p) return fail(RLK_EINVAL, "params is NULL");
+  if (!W || !dW || !loss) return fail(RLK_EINVAL, "W, dW or loss is NULL");
+  if (b->N > 0 && (!hidden || !targets || !old_logp || !dhidden))
+    return fail(RLK_EINVAL, "hidden, targets, old_logp or dhidden is NULL");
+  if (b->R > 0 && (!rewards || !group_ids)) return fail(RLK_EINVAL, "rewards or group_ids is NULL");
+  if (!(p->eps_low >= 0.0f && p->eps_low < 1.0f) || !(p->eps_high >= 0.0f) || !isfinite(p->eps_high))
+    return fail(RLK_EINVAL, "clip range must satisfy 0 <= eps_low < 1 and finite eps_high >= 0");
+  if (!(p->adv_eps >= 0.0f) || !isfinite(p->adv_eps)) return fail(RLK_EINVAL, "adv_eps must be finite and >= 0");
+  if (!isfinite(p->entropy_coef)) return fail(RLK_EINVAL, "entropy_coef must be finite");
+  if (p->agg != RLK_AGG_SEQ_MEAN_TOKEN_MEAN && p->agg != RLK_AGG_TOKEN_MEAN)
+    return fail(RLK_EINVAL, "unknown aggregation %d", p->agg);
+  if (p->accumulate_dW != 0 && p->accumulate_dW != 1) return fail(RLK_EINVAL, "accumulate_dW must be 0 or 1");
+  if (!(p->norm_override >= 0.0) || !isfinite(p->norm_override))
+    return fail(RLK_EINVAL, "norm_override must be finite and >= 0");
+  for (int i = 0; i < 4; ++i)
+    if (p->reserved[i] != 0) return fail(RLK_EINVAL, "reserved parameter fields must be 0");
+  WsLayout L;
+  st = layout(b, true, p->chunk_rows, L);
+  if (st) return st;
+  st = check_ws(ws, ws_bytes, L.total);
+  if (st) return st;
+
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  char* w = static_cast<char*>(ws);
+  WsHeader* hdr = reinterpret_cast<WsHeader*>(w + L.hdr);
+  const int64_t N = b->N;
+  const int R = b->R;
+  auto F = [&](size_t off) { return reinterpret_cast<float*>(w + off); };
+  auto I = [&](size_t off) { return reinterpret_cast<int32_t*>(w + off); };
+
+  RLK_TRY(launch_begin(reinterpret_cast<int32_t*>(hdr), b->cu_seqlens, R, N, s), "begin");
+  RLK_TRY(launch_compact(mask, b->cu_seqlens, group_ids, R, N, targets, b->V, w, L, s), "compact");
+  RLK_TRY(launch_advantage(R, rewards, group_ids, p->adv_eps, I(L.first), I(L.gidx), I(L.gsize),
+                           reinterpret_cast<double*>(w + L.gmu), reinterpret_cast<double*>(w + L.gsig), I(L.geq),
+                           F(L.adv), hdr, s),
+          "advantage");
+  RLK_TRY(launch_transpose_w(b->dtype, W, w + L.wt, b->V, L.Vp, b->d, s), "transpose_w");
+  for (int c = 0; c < L.nchunks; ++c) {
+    const int64_t c0 = (int64_t)c * L.Mc;
+    RLK_TRY(launch_gather(b->dtype, hidden, b->d, I(L.idx), hdr, c0, L.Mc, w + L.hc, w + L.ht, true, s), "gather");
+    GemmArgs g = {};
+    g.A = W;
+    g.B = w + L.hc;
+    g.lda = b->d;
+    g.ldb = b->d;
+    g.M = b->V;
+    g.N = (int)L.Mc;
+    g.K = b->d;
+    g.hdr = hdr;
+    g.c0 = c0;
+    g.Mc = L.Mc;
+    g.ytgt = I(L.ytgt);
+    g.zy = F(L.zy);
+    g.pm = F(L.pm);
+    g.ps = F(L.ps);
+    g.pu = F(L.pu);
+    g.q = w + L.q;
+    g.ldq = L.Vp;
+    g.V = b->V;
+    RLK_TRY(launch_fwd_gemm(b->dtype, g, true, s), "fwd_gemm");
+
+    TokenParams tp = {};
+    tp.hdr = hdr;
+    tp.c0 = c0;
+    tp.Mc = L.Mc;
+    tp.nvt = L.nvt;
+    tp.pm = g.pm;
+    tp.ps = g.ps;
+    tp.pu = g.pu;
+    tp.zy = g.zy;
+    tp.idx = I(L.idx);
+    tp.tokr = I(L.tokr);
+    tp.ytgt = I(L.ytgt);
+    tp.lse = F(L.lse);
+    tp.logp = F(L.logp);
+    tp.ent = F(L.ent);
+    tp.gt = F(L.gt);
+    tp.et = F(L.et);
+    tp.logp_out = logp_out;
+    tp.ent_out = entropy_out;
+    tp.with_grad = 1;
+    tp.old_logp = old_logp;
+    tp.adv = F(L.adv);
+    tp.rnpol = I(L.rnpol);
+    tp.gidx = I(L.gidx);
+    tp.gsize = I(L.gsize);
+    tp.eps_low = p->eps_low;
+    tp.eps_high = p->eps_high;
+    tp.ent_coef = p->entropy_coef;
+    tp.agg = p->agg;
+    tp.norm_override = p->norm_override;
+    RLK_TRY(launch_combine(tp, s), "combine");
+
+    DzParams dp = {};
+    dp.hdr = hdr;
+    dp.c0 = c0;
+    dp.Mc = L.Mc;
+    dp.Vp = L.Vp;
+    dp.V = b->V;
+    dp.q = w + L.q;
+    dp.dzt = w + L.dzt;
+    dp.pm = g.pm;
+    dp.lse = tp.lse;
+    dp.logp = tp.logp;
+    dp.ent = tp.ent;
+    dp.gt = tp.gt;
+    dp.et = tp.et;
+    dp.ytgt = tp.ytgt;
+    dp.has_ent = p->entropy_coef != 0.0f;
+    RLK_TRY(launch_dz(b->dtype, dp, s), "dz");
+
+    GemmArgs h = {};
+    h.A = w + L.q;
+    h.B = w + L.wt;
+    h.lda = L.Vp;
+    h.ldb = L.Vp;
+    h.M = (int)L.Mc;
+    h.N = b->d;
+    h.K = (int)L.Vp;
+    h.hdr = hdr;
+    h.c0 = c0;
+    h.Mc = L.Mc;
+    h.out = dhidden;
+    h.idx = I(L.idx);
+    h.ldo = b->d;
+    RLK_TRY(launch_dh_gemm(b->dtype, h, s), "dh_gemm");
+
+    GemmArgs k = {};
+    k.A = w + L.dzt;
+    k.B = w + L.ht;
+    k.lda = L.Mc;
+    k.ldb = L.Mc;
+    k.M = b->V;
+    k.N = b->d;
+    k.K = (int)L.Mc;
+    k.hdr = hdr;
+    k.c0 = c0;
+    k.Mc = L.Mc;
+    k.dw = dW;
+    k.ldo = b->d;
+    k.accumulate = p->accumulate_dW;
+    RLK_TRY(launch_dw_gemm(b->dtype, k, s), "dw_gemm");
+  }
+
+  LossParams lp = {};
+  lp.hdr = hdr;
+  lp.R = R;
+  lp.rstart = I(L.rstart);
+  lp.rnpol = I(L.rnpol);
+  lp.gidx = I(L.gidx);
+  lp.gsize = I(L.gsize);
+  lp.idx = I(L.idx);
+  lp.logp = F(L.logp);
+  lp.ent = F(L.ent);
+  lp.old_logp = old_logp;
+  lp.adv = F(L.adv);
+  lp.rsum = reinterpret_cast<double*>(w + L.rsum);
+  lp.eps_low = p->eps_low;
+  lp.eps_high = p->eps_high;
+  lp.ent_coef = p->entropy_coef;
+  lp.agg = p->agg;
+  lp.norm_override = p->norm_override;
+  lp.loss = loss;
+  lp.stats = stats;
+  RLK_TRY(launch_loss(lp, s, 0), "loss");
+  RLK_TRY(launch_zero_fill(b->dtype, reinterpret_cast<const uint8_t*>(w + L.keep), N, b->d, dhidden, logp_out,
+                           entropy_out, nullptr, s),
+          "zero_fill");
+  return finish(hipSuccess, "", ws, s);
+}
+
+rlk_status_t rlk_check_status(const void* ws, void* stream, int32_t* flags) {
+  if (!ws) return fail(RLK_EINVAL, "workspace is NULL");
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  RLK_TRY(hipStreamSynchronize(s), "hipStreamSynchronize");
+  int32_t st = 0;
+  RLK_TRY(hipMemcpy(&st, ws, sizeof(int32_t), hipMemcpyDeviceToHost), "hipMemcpy(status)");
+  if (flags) *flags = st;
+  if (st != 0) return fail(RLK_EDATA, "device data error flags 0x%x", st);
+  return RLK_OK;
+}
+
+const char* rlk_status_string(rlk_status_t s) {
+  switch (s) {
+    case RLK_OK: return "ok";
+    case RLK_EINVAL: return "invalid argument";
+    case RLK_ESHAPE: return "unsupported or inconsistent shape";
+    case RLK_EDTYPE: return "unknown dtype";
+    case RLK_EWORKSPACE: return "workspace missing, misaligned or too small";
+    case RLK_EHIP: return "HIP runtime error";
+    case RLK_EDATA: return "device data error";
+    default: return "unknown status";
+  }
+}
+
+const char* rlk_last_error(void) { return g_last_error.c_str(); }
+
+int32_t rlk_version(void) { return RLK_VERSION; }
+
+rlk_status_t rlk_profile_begin(void) {
+  Prof& P = prof();
+  std::lock_guard<std::mutex> lk(P.mu);
+  for (auto& r : P.recs) {
+    (void)hipEventDestroy(r.a);
+    (void)hipEventDestroy(r.b);
+  }
+  P.recs.clear();
+  P.on = true;
+  return RLK_OK;
+}
+
+rlk_status_t rlk_profile_end(int32_t max_kinds, double* total_ms, int32_t* launches, int32_t* n_kinds) {
+  Prof& P = prof();
+  std::lock_guard<std::mutex> lk(P.mu);
+  P.on = false;
+  if (n_kinds) *n_kinds = KK_COUNT_KINDS;
+  for (int k = 0; k < max_kinds && k < KK_COUNT_KINDS; ++k) {
+    if (total_ms) total_ms[k] = 0.0;
+    if (launches) launches[k] = 0;
+  }
+  rlk_status_t rc = RLK_OK;
+  for (auto& r : P.recs) {
+    float ms = 0.0f;
+    if (hipEventSynchronize(r.b) != hipSuccess || hipEventElapsedTime(&ms, r.a, r.b) != hipSuccess) {
+      rc = fail(RLK_EHIP, "event timing failed");
+    } else if (r.kind < max_kinds) {
+      if (total_ms) total_ms[r.kind] += ms;
+      if (launches) launches[r.kind] += 1;
+    }
+    (void)hipEventDestroy(r.a);
+    (void)hipEventDestroy(r.b);
+  }
+  P.recs.clear();
+  return rc;
+}
+
+const char* rlk_kernel_kind_name(int32_t kind) {
+  if (kind < 0 || kind >= KK_COUNT_KINDS) return "";
+  return kKindNames[kind];
+}
+
+}  // extern "C"

@@ -1,0 +1,179 @@
+// Internal declarations shared by the HIP translation units of librlk.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "../../include/rlk.h"
+
+namespace rlk {
+
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+// Storage type of a bf16 element (bit pattern).
+struct bf16_t {
+  uint16_t bits;
+};
+
+// Tile geometry of the MFMA GEMMs (see k_gemm.hip).
+constexpr int kTile = 256;       // BM = BN = 256
+constexpr int kVocabTile = 256;  // vocabulary rows per forward tile = per online-LSE partial
+constexpr int kChunkAlign = 256; // chunk_rows granularity
+constexpr int kKAlign = 64;      // K padding of the chunk buffers (bf16 elements per stage)
+constexpr int kScanTile = 4096;  // tokens per compaction block
+constexpr int kMaxRollouts = 16384;
+
+enum KernelKind {
+  KK_BEGIN = 0,
+  KK_COUNT,
+  KK_SCAN,
+  KK_WRITE_IDX,
+  KK_ROLLOUT_OFFSETS,
+  KK_GROUP_RANK,
+  KK_GROUP_STATS,
+  KK_ADVANTAGE,
+  KK_TRANSPOSE_W,
+  KK_GATHER,
+  KK_FWD_GEMM,
+  KK_COMBINE,
+  KK_DZ,
+  KK_DH_GEMM,
+  KK_DW_GEMM,
+  KK_LOSS_ROLLOUT,
+  KK_LOSS_FINAL,
+  KK_ZERO_FILL,
+  KK_COUNT_KINDS
+};
+
+// Device-side header at offset 0 of every workspace.
+struct WsHeader {
+  int32_t status;    // RLK_DERR_* bits
+  int32_t n_eff;     // number of trained tokens
+  int32_t n_groups;  // Q
+  int32_t n_valid;   // non-excluded rollouts
+  int32_t pad[60];
+};
+
+// Byte offsets of the workspace segments (all 256-aligned).
+struct WsLayout {
+  size_t total = 0;
+  size_t hdr = 0;
+  // token arrays [N]
+  size_t keep = 0, idx = 0, tokr = 0, ytgt = 0, zy = 0, lse = 0, logp = 0, ent = 0, gt = 0, et = 0;
+  // compaction block scan [nblk]
+  size_t blkcnt = 0, blkoff = 0;
+  // rollouts [R]
+  size_t rstart = 0, rnpol = 0, first = 0, gidx = 0, gsize = 0, gmu = 0, gsig = 0, geq = 0, adv = 0;
+  size_t rsum = 0;  // double [R][4]
+  // chunk buffers
+  size_t pm = 0, ps = 0, pu = 0;   // float [nvt][Mc]
+  size_t hc = 0;                   // T [Mc][d]
+  size_t ht = 0;                   // T [d][Mc]
+  size_t q = 0;                    // T [Mc][Vp]
+  size_t dzt = 0;                  // T [Vp][Mc]
+  size_t wt = 0;                   // T [d][Vp]
+  int64_t Mc = 0;                  // chunk rows
+  int64_t Vp = 0;                  // vocabulary padded to 256
+  int32_t nvt = 0;                 // vocabulary tiles
+  int32_t nblk = 0;                // compaction blocks
+  int32_t nchunks = 0;             // chunk iterations launched (ceil(N / Mc))
+};
+
+// ---- launchers (k_segment.hip) ----
+hipError_t launch_begin(int32_t* status_hdr, const int32_t* cu, int R, int64_t N, hipStream_t s);
+hipError_t launch_compact(const uint8_t* mask, const int32_t* cu, const int32_t* gid, int R, int64_t N,
+                          const int32_t* targets, int V, char* ws, const WsLayout& L, hipStream_t s);
+hipError_t launch_advantage(int R, const float* rewards, const int32_t* gid, float adv_eps,
+                            int32_t* first, int32_t* gidx, int32_t* gsize, double* gmu, double* gsig,
+                            int32_t* geq, float* adv, WsHeader* hdr, hipStream_t s);
+
+// ---- launchers (k_token.hip) ----
+hipError_t launch_transpose_w(int dtype, const void* W, void* WT, int V, int64_t Vp, int d, hipStream_t s);
+hipError_t launch_gather(int dtype, const void* hidden, int d, const int32_t* idx, const WsHeader* hdr,
+                         int64_t c0, int64_t Mc, void* hc, void* ht, bool want_ht, hipStream_t s);
+
+struct TokenParams {
+  const WsHeader* hdr;
+  int64_t c0, Mc;
+  int nvt;
+  const float *pm, *ps, *pu, *zy;
+  const int32_t *idx, *tokr, *ytgt;
+  float *lse, *logp, *ent, *gt, *et;
+  float *logp_out, *ent_out, *lse_out;   // scattered [N] outputs, may be null
+  // loss terms (fwd+bwd only)
+  int with_grad;
+  const float* old_logp;
+  const float* adv;
+  const int32_t *rnpol, *gidx, *gsize;
+  float eps_low, eps_high, ent_coef;
+  int agg;
+  double norm_override;
+};
+hipError_t launch_combine(const TokenParams& p, hipStream_t s);
+
+struct DzParams {
+  const WsHeader* hdr;
+  int64_t c0, Mc, Vp;
+  int V;
+  void* q;        // in: exp(z - m_tile) ; out: dz, [Mc][Vp]
+  void* dzt;      // out: dz transposed, [Vp][Mc]
+  const float *pm, *lse, *logp, *ent, *gt, *et;
+  const int32_t* ytgt;
+  int has_ent;
+};
+hipError_t launch_dz(int dtype, const DzParams& p, hipStream_t s);
+
+struct LossParams {
+  const WsHeader* hdr;
+  int R;
+  const int32_t *rstart, *rnpol, *gidx, *gsize, *idx;
+  const float *logp, *ent, *old_logp, *adv;
+  double* rsum;
+  float eps_low, eps_high, ent_coef;
+  int agg;
+  double norm_override;
+  float* loss;
+  rlk_pg_stats_t* stats;
+};
+hipError_t launch_loss(const LossParams& p, hipStream_t s, int prof_kind_first);
+
+hipError_t launch_zero_fill(int dtype, const uint8_t* keep, int64_t N, int d, void* dh, float* o1, float* o2,
+                            float* o3, hipStream_t s);
+
+// ---- launchers (k_gemm.hip) ----
+struct GemmArgs {
+  const void* A;
+  const void* B;
+  int64_t lda, ldb;      // elements
+  int M, N, K;           // static maxima (the data-dependent one is derived on device)
+  const WsHeader* hdr;   // n_eff
+  int64_t c0;            // first compacted row of the chunk
+  int64_t Mc;            // chunk capacity
+  // forward epilogue
+  const int32_t* ytgt;   // compacted targets
+  float* zy;
+  float *pm, *ps, *pu;   // [nvt][Mc]
+  void* q;               // [Mc][ldq]
+  int64_t ldq;
+  int V;
+  // dhidden epilogue
+  void* out;
+  const int32_t* idx;
+  int64_t ldo;
+  // dW epilogue
+  float* dw;
+  int accumulate;
+};
+hipError_t launch_fwd_gemm(int dtype, const GemmArgs& a, bool store_q, hipStream_t s);
+hipError_t launch_dh_gemm(int dtype, const GemmArgs& a, hipStream_t s);
+hipError_t launch_dw_gemm(int dtype, const GemmArgs& a, hipStream_t s);
+
+// ---- profiling (rlk_api.hip) ----
+void prof_mark(int kind, bool begin, hipStream_t s);
+
+}  // namespace rlk

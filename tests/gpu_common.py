@@ -1,0 +1,152 @@
+"""Shared helpers of the GPU parity tests: seeded instances on the device, the call into the
+HIP library through the C ABI, and the comparison metrics.  Expected values always come
+from the fp64 oracle run on host copies of exactly the bytes the GPU consumed."""
+from __future__ import annotations
+
+import math
+import os
+import sys
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+import oracle as O  # noqa: E402
+import paper_2608_16798_amd as rlk  # noqa: E402
+import workloads as WL  # noqa: E402
+from workloads.anchor import gaussian_anchor  # noqa: E402
+
+# Tolerances (per-token log-prob: abs; loss: relative to the L1 size of its terms; gradients:
+# relative Frobenius).  fp32 configurations use the tighter log-prob bound.
+TOL_LOGP = {"f32": 1e-4, "bf16": 3e-2}
+TOL_LOSS = 1e-3
+TOL_GRAD = 2e-2
+
+
+def log(*a):
+    print(*a, flush=True)
+
+
+def ensure_library():
+    if not os.path.exists(rlk.LIB_PATH):
+        from paper_2608_16798_amd.build import build
+
+        build(verbose=False)
+    return rlk.load_library()
+
+
+def to_host(t):
+    import torch
+
+    if t.dtype == torch.bfloat16:
+        return t.float().cpu().numpy()
+    return t.cpu().numpy()
+
+
+def build_instance(cfg, device="cuda", structure=None):
+    """Seeded instance of a configuration on the device, plus host copies for the oracle."""
+    import torch
+
+    st = structure if structure is not None else WL.make_structure(cfg)
+    h, W = WL.make_tensors(cfg, st.N, device=device)
+    if cfg.anchor == "oracle":
+        _, anchor, _ = O.token_logprob(to_host(h), to_host(W), st.targets)
+    else:
+        anchor = gaussian_anchor(h, W, st.targets, cfg.w_std)
+    old = WL.old_logp_from_anchor(anchor, st)
+    dev = lambda a, dt: torch.as_tensor(a, dtype=dt, device=device)
+    inst = dict(
+        cfg=cfg, st=st, h=h, W=W,
+        cu=dev(st.cu_seqlens, torch.int32), mask=dev(st.mask, torch.uint8),
+        targets=dev(st.targets, torch.int32), rewards=dev(st.rewards, torch.float32),
+        gid=dev(st.group_ids, torch.int32), old=dev(old, torch.float32), old_host=old)
+    return inst
+
+
+def params_for(cfg, **kw):
+    base = dict(eps_low=cfg.eps_low, eps_high=cfg.eps_high, entropy_coef=cfg.entropy_coef)
+    base.update(kw)
+    return rlk.make_params(**base)
+
+
+def run_gpu(inst, params, *, gid=None, mask="default", dW=None, ws=None):
+    import torch
+
+    h, W = inst["h"], inst["W"]
+    N = h.shape[0]
+    logp = torch.empty(N, dtype=torch.float32, device=h.device)
+    ent = torch.empty(N, dtype=torch.float32, device=h.device)
+    stats = rlk.stats_buffer(h.device)
+    loss, dh, dWo, ws = rlk.pg_loss_fwd_bwd(
+        h, W, inst["targets"], inst["mask"] if mask == "default" else mask, inst["cu"], inst["old"],
+        inst["rewards"], inst["gid"] if gid is None else gid, params, dW=dW, logp_out=logp, entropy_out=ent,
+        stats=stats, ws=ws)
+    torch.cuda.synchronize()
+    flags = rlk.check_status(ws)
+    return dict(loss=float(loss.item()), dh=dh, dW=dWo, logp=logp, ent=ent, stats=rlk.stats_from_tensor(stats),
+                flags=flags, ws=ws)
+
+
+def run_oracle(inst, params, *, grads=True):
+    st = inst["st"]
+    return O.pg_loss_fwd_bwd(
+        to_host(inst["h"]), to_host(inst["W"]), st.targets, st.mask, st.cu_seqlens, inst["old_host"],
+        st.rewards, st.group_ids, eps_low=params.eps_low, eps_high=params.eps_high, adv_eps=params.adv_eps,
+        entropy_coef=params.entropy_coef, agg=params.agg,
+        norm_override=params.norm_override if params.norm_override > 0 else None, grads=grads)
+
+
+def rel_fro(a, b):
+    a = np.asarray(a, dtype=np.float64)
+    b = np.asarray(b, dtype=np.float64)
+    nb = np.linalg.norm(b)
+    return float(np.linalg.norm(a - b) / (nb if nb > 0 else 1.0))
+
+
+def loss_scale(ref, params):
+    """L1 size of the loss terms: sum_t |w_t (s_t + c H_t)|."""
+    A = ref["adv"][ref["tok_rollout"]]
+    rho = ref["rho"]
+    c = np.clip(rho, 1 - params.eps_low, 1 + params.eps_high)
+    sv = np.minimum(rho * A, c * A) + params.entropy_coef * ref["H"]
+    return float(np.abs(ref["omega"] * sv).sum())
+
+
+def compare_full(inst, gpu, ref, params, tag=""):
+    """Element-wise parity of every output against the oracle; returns the metrics."""
+    cfg = inst["cfg"]
+    idx = ref["idx"]
+    N = inst["h"].shape[0]
+    keep = np.zeros(N, dtype=bool)
+    keep[idx] = True
+    logp = gpu["logp"].cpu().numpy()
+    ent = gpu["ent"].cpu().numpy()
+    m = {}
+    m["logp_abs"] = float(np.abs(logp[idx] - ref["logp"]).max()) if idx.size else 0.0
+    m["ent_abs"] = float(np.abs(ent[idx] - ref["H"]).max()) if idx.size else 0.0
+    m["masked_nonzero"] = int((logp[~keep] != 0).sum() + (ent[~keep] != 0).sum())
+    scale = loss_scale(ref, params)
+    m["loss_gpu"], m["loss_ref"] = gpu["loss"], ref["loss"]
+    m["loss_rel_l1"] = abs(gpu["loss"] - ref["loss"]) / max(scale, 1e-30) if scale > 0 else abs(gpu["loss"])
+    m["loss_rel"] = abs(gpu["loss"] - ref["loss"]) / max(abs(ref["loss"]), 1e-30)
+    dh = to_host(gpu["dh"])
+    m["dh_rel"] = rel_fro(dh[idx], ref["dh"][idx])
+    m["dh_masked_nonzero"] = int(np.count_nonzero(dh[~keep]))
+    m["dW_rel"] = rel_fro(to_host(gpu["dW"]), ref["dW"])
+    st = gpu["stats"]
+    m["stats_ok"] = (st["n_policy_tokens"] == ref["stats"]["n_policy_tokens"]
+                     and st["n_groups"] == ref["stats"]["n_groups"]
+                     and st["n_valid_rollouts"] == ref["stats"]["n_valid_rollouts"])
+    m["flags"] = gpu["flags"]
+    log(f"[{tag}] {cfg.name}: " + ", ".join(f"{k}={v:.3g}" if isinstance(v, float) else f"{k}={v}"
+                                            for k, v in m.items()))
+    tl = TOL_LOGP[cfg.dtype]
+    assert m["flags"] == 0
+    assert m["logp_abs"] <= tl and m["ent_abs"] <= tl
+    assert m["masked_nonzero"] == 0 and m["dh_masked_nonzero"] == 0
+    assert m["loss_rel_l1"] <= TOL_LOSS
+    assert m["dh_rel"] <= TOL_GRAD and m["dW_rel"] <= TOL_GRAD
+    assert m["stats_ok"]
+    return m

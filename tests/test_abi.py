@@ -1,0 +1,109 @@
+"""Host-side checks of the C ABI: the library loads, exports every declared entry point,
+sizes workspaces and rejects invalid arguments before launching anything (no GPU needed)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2608_16798_amd as rlk
+from workloads import get_config
+from workloads.configs import ORDER
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(rlk.LIB_PATH):
+        from paper_2608_16798_amd.build import build
+
+        build(verbose=False)
+    return rlk.load_library()
+
+
+def declared_functions():
+    src = open(os.path.join(ROOT, "include", "rlk.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(rlk_[a-z_]+)\s*\(", src)))
+
+
+def test_exports_every_declared_symbol(lib):
+    names = declared_functions()
+    assert "rlk_pg_loss_fwd_bwd" in names and "rlk_logprob_fwd" in names and "rlk_group_advantage" in names
+    for n in names:
+        assert hasattr(lib, n), n
+    assert set(names) == set(rlk.EXPORTS)
+
+
+def test_version_and_strings(lib):
+    assert lib.rlk_version() == 1
+    assert lib.rlk_status_string(rlk.RLK_EWORKSPACE).decode().startswith("workspace")
+    assert lib.rlk_kernel_kind_name(10).decode() == "fwd_lse_gemm"
+
+
+def _batch(cfg, N=4096, R=8, cu=0x1000):
+    return rlk.Batch(N=N, R=R, d=cfg.d, V=cfg.V, dtype=rlk.DTYPE_BF16 if cfg.dtype == "bf16" else rlk.DTYPE_F32,
+                     cu_seqlens=cu)
+
+
+@pytest.mark.parametrize("name", ORDER)
+def test_workspace_sizes(lib, name):
+    cfg = get_config(name)
+    b = _batch(cfg)
+    fwd = rlk.workspace_size(b)
+    bwd = rlk.workspace_size(b, rlk.make_params())
+    assert 0 < fwd < bwd
+    esz = 2 if cfg.dtype == "bf16" else 4
+    Vp = (cfg.V + 255) // 256 * 256
+    Mc = 4096  # chunk capped at the token count rounded to 256
+    assert bwd >= 2 * Mc * Vp * esz + cfg.d * Vp * esz
+    big = rlk.workspace_size(b, rlk.make_params(chunk_rows=8192))
+    assert big > bwd
+
+
+def test_host_validation(lib):
+    cfg = get_config("tiny_fp32")
+    n = ctypes.c_size_t()
+    b = _batch(cfg)
+    assert lib.rlk_workspace_size(None, None, ctypes.byref(n)) == rlk.RLK_EINVAL
+    bad = _batch(cfg)
+    bad.dtype = 7
+    assert lib.rlk_workspace_size(ctypes.byref(bad), None, ctypes.byref(n)) == rlk.RLK_EDTYPE
+    bad = _batch(cfg)
+    bad.d = 12
+    assert lib.rlk_workspace_size(ctypes.byref(bad), None, ctypes.byref(n)) == rlk.RLK_ESHAPE
+    assert b"multiple of 8" in lib.rlk_last_error()
+    bad = _batch(cfg, N=10, R=0)
+    assert lib.rlk_workspace_size(ctypes.byref(bad), None, ctypes.byref(n)) == rlk.RLK_ESHAPE
+    p = rlk.make_params(chunk_rows=300)
+    assert lib.rlk_workspace_size(ctypes.byref(b), ctypes.byref(p), ctypes.byref(n)) == rlk.RLK_ESHAPE
+    assert lib.rlk_advantage_workspace_size(20000, ctypes.byref(n)) == rlk.RLK_ESHAPE
+
+    fake = 0x10000  # never dereferenced: every call below fails validation first
+    need = rlk.workspace_size(b)
+    # missing / misaligned / short workspace
+    assert lib.rlk_logprob_fwd(ctypes.byref(b), fake, fake, fake, None, fake, None, None, None, need, None) \
+        == rlk.RLK_EWORKSPACE
+    assert lib.rlk_logprob_fwd(ctypes.byref(b), fake, fake, fake, None, fake, None, None, fake + 8, need, None) \
+        == rlk.RLK_EWORKSPACE
+    assert lib.rlk_logprob_fwd(ctypes.byref(b), fake, fake, fake, None, fake, None, None, fake, need - 1, None) \
+        == rlk.RLK_EWORKSPACE
+    assert lib.rlk_logprob_fwd(ctypes.byref(b), None, fake, fake, None, fake, None, None, fake, need, None) \
+        == rlk.RLK_EINVAL
+    # loss parameters
+    args = lambda p: (ctypes.byref(b), fake, fake, fake, None, fake, fake, fake, ctypes.byref(p), fake, fake, fake,
+                      None, None, None, fake, 1 << 40, None)
+    for kw in (dict(eps_low=1.0), dict(eps_low=-0.1), dict(agg=3), dict(adv_eps=-1.0)):
+        p = rlk.make_params(**kw)
+        assert lib.rlk_pg_loss_fwd_bwd(*args(p)) == rlk.RLK_EINVAL, kw
+    p = rlk.make_params()
+    p.reserved[2] = 1
+    assert lib.rlk_pg_loss_fwd_bwd(*args(p)) == rlk.RLK_EINVAL
+    p = rlk.make_params()
+    p.accumulate_dW = 2
+    assert lib.rlk_pg_loss_fwd_bwd(*args(p)) == rlk.RLK_EINVAL
+    assert lib.rlk_group_advantage(8, fake, fake, ctypes.c_float(-1.0), fake, None, None, fake, 1 << 20, None) \
+        == rlk.RLK_EINVAL
+    assert lib.rlk_group_advantage(8, None, fake, ctypes.c_float(1e-6), fake, None, None, fake, 1 << 20, None) \
+        == rlk.RLK_EINVAL

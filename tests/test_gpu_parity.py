@@ -1,0 +1,300 @@
+"""GPU parity of the HIP hot path against the fp64 oracle, through the C ABI.
+
+Integer outputs (compaction lists, group indices, counts) must be bit-exact; floating
+outputs meet the tolerances in gpu_common.  Full parity runs on every configuration at a
+scaled size the oracle finishes in seconds (several token and vocabulary tiles, ragged
+tails, several backward chunks); the full-size runs are checked on seeded sampled rows
+that the oracle computes one by one and on properties that hold at any size.
+"""
+import numpy as np
+import pytest
+
+from gpu_common import (TOL_GRAD, TOL_LOGP, O, WL, build_instance, compare_full, ensure_library, log,
+                        params_for, rel_fro, rlk, run_gpu, run_oracle, to_host)
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _lib():
+    import torch
+
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    ensure_library()
+
+
+def _dev(a, dt):
+    import torch
+
+    return torch.as_tensor(a, dtype=dt, device="cuda")
+
+
+# ------------------------------------------------------------------ a1: compaction (bit-exact)
+@pytest.mark.parametrize("name,scaled,excl", [("tiny_fp32", False, 0), ("qwen8b_bf16", False, 3),
+                                               ("large_bf16", False, 7), ("long_bf16", True, 1)])
+def test_compaction_bit_exact(name, scaled, excl):
+    import torch
+
+    cfg = WL.scaled_config(name) if scaled else WL.get_config(name)
+    cfg = cfg.with_(n_excluded=excl)
+    st = WL.make_structure(cfg)
+    log(f"compaction {cfg.name} N={st.N} R={st.R} excluded={excl}")
+    idx, tokr, npol, neff, ws = rlk.compact(_dev(st.cu_seqlens, torch.int32), _dev(st.mask, torch.uint8),
+                                            _dev(st.group_ids, torch.int32), _dev(st.targets, torch.int32),
+                                            V=cfg.V)
+    torch.cuda.synchronize()
+    ri, rt, rn = O.compact(st.mask, st.cu_seqlens, st.group_ids)
+    n = int(neff.item())
+    assert n == ri.shape[0]
+    assert np.array_equal(idx[:n].cpu().numpy(), ri)
+    assert np.array_equal(tokr[:n].cpu().numpy(), rt)
+    assert np.array_equal(npol.cpu().numpy(), rn)
+    assert rlk.check_status(ws) == 0
+
+
+def test_compaction_edge_cases():
+    import torch
+
+    # empty rollouts, a rollout of length 1, all-masked rollout, mask NULL
+    lens = np.array([0, 1, 5, 0, 300, 4096, 4097, 2])
+    cu = np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)
+    N = int(cu[-1])
+    rng = np.random.default_rng(5)
+    mask = (rng.random(N) < 0.5).astype(np.uint8)
+    mask[cu[4]:cu[5]] = 0
+    gid = np.array([3, 3, 0, 9, 9, -1, 0, 3], dtype=np.int32)
+    for m in (mask, None):
+        idx, tokr, npol, neff, ws = rlk.compact(_dev(cu, torch.int32), None if m is None else _dev(m, torch.uint8),
+                                                _dev(gid, torch.int32), N=N)
+        ri, rt, rn = O.compact(m, cu, gid)
+        n = int(neff.item())
+        assert n == len(ri)
+        assert np.array_equal(idx[:n].cpu().numpy(), ri) and np.array_equal(tokr[:n].cpu().numpy(), rt)
+        assert np.array_equal(npol.cpu().numpy(), rn)
+
+
+# ------------------------------------------------------------------ a2: advantages
+@pytest.mark.parametrize("name,excl", [("large_bf16", 5), ("qwen8b_bf16", 0), ("tiny_fp32", 1)])
+def test_group_advantage(name, excl):
+    import torch
+
+    cfg = WL.get_config(name).with_(n_excluded=excl)
+    st = WL.make_structure(cfg)
+    R = st.R
+    gi = torch.empty(R, dtype=torch.int32, device="cuda")
+    ng = torch.empty(1, dtype=torch.int32, device="cuda")
+    adv = rlk.group_advantage(_dev(st.rewards, torch.float32), _dev(st.group_ids, torch.int32), 1e-6,
+                              group_index=gi, n_groups=ng)
+    ref = O.group_advantage(st.rewards, st.group_ids, 1e-6)
+    a = adv.cpu().numpy()
+    assert np.array_equal(gi.cpu().numpy(), ref["group_index"])
+    assert int(ng.item()) == ref["n_groups"]
+    err = np.abs(a - ref["adv"]).max()
+    log(f"advantage {name}: max abs err {err:.3g}")
+    assert err <= 1e-6 * max(1.0, np.abs(ref["adv"]).max())
+    # all-equal groups and excluded rollouts are exactly zero
+    zero = np.flatnonzero(ref["adv"] == 0)
+    assert np.all(a[zero] == 0)
+
+
+def test_group_advantage_small_cases():
+    import torch
+
+    rew = np.array([1, 0, 0, 0, 0.5, 0.5, 7, 1, 0], dtype=np.float32)
+    gid = np.array([2, 2, 2, 2, 5, 5, 0, -1, 11], dtype=np.int32)
+    adv = rlk.group_advantage(_dev(rew, torch.float32), _dev(gid, torch.int32), 1e-6).cpu().numpy()
+    p = 0.25
+    s = np.sqrt(p * (1 - p))
+    np.testing.assert_allclose(adv[:4], [(1 - p) / (s + 1e-6)] + [-p / (s + 1e-6)] * 3, rtol=1e-6)
+    assert np.all(adv[4:] == 0)
+
+
+# ------------------------------------------------------------------ a3: log-prob forward
+@pytest.mark.parametrize("name,scaled", [("tiny_fp32", False), ("small_bf16", True), ("qwen8b_bf16", True)])
+def test_logprob_fwd(name, scaled):
+    import torch
+
+    cfg = WL.scaled_config(name) if scaled else WL.get_config(name)
+    st = WL.make_structure(cfg)
+    h, W = WL.make_tensors(cfg, st.N, device="cuda")
+    N = st.N
+    log(f"logprob {cfg.name} N={N} d={cfg.d} V={cfg.V}")
+    ent = torch.empty(N, dtype=torch.float32, device="cuda")
+    lse = torch.empty(N, dtype=torch.float32, device="cuda")
+    logp, _, _, ws = rlk.logprob_fwd(h, W, _dev(st.targets, torch.int32), _dev(st.mask, torch.uint8),
+                                     _dev(st.cu_seqlens, torch.int32), entropy=ent, lse=lse)
+    torch.cuda.synchronize()
+    assert rlk.check_status(ws) == 0
+    idx, _, _ = O.compact(st.mask, st.cu_seqlens)
+    rl, rp, rH = O.token_logprob(to_host(h)[idx], to_host(W), st.targets[idx])
+    g = {k: v.cpu().numpy() for k, v in (("logp", logp), ("ent", ent), ("lse", lse))}
+    e = dict(logp=np.abs(g["logp"][idx] - rp).max(), ent=np.abs(g["ent"][idx] - rH).max(),
+             lse=np.abs(g["lse"][idx] - rl).max())
+    log(f"  max abs err {e}")
+    tol = TOL_LOGP[cfg.dtype]
+    assert e["logp"] <= tol and e["ent"] <= tol and e["lse"] <= tol * max(1.0, np.abs(rl).max())
+    keep = np.zeros(N, dtype=bool)
+    keep[idx] = True
+    for k in g:
+        assert np.all(g[k][~keep] == 0)
+
+
+# ------------------------------------------------------------------ a1-a7: loss forward + backward
+PARITY = [("tiny_fp32", False, 0), ("small_bf16", True, 0), ("qwen8b_bf16", True, 256),
+          ("long_bf16", True, 512), ("large_bf16", True, 256)]
+
+
+@pytest.mark.parametrize("name,scaled,chunk", PARITY)
+def test_pg_loss_parity(name, scaled, chunk):
+    cfg = WL.scaled_config(name) if scaled else WL.get_config(name)
+    if name == "large_bf16":
+        cfg = cfg.with_(n_excluded=1)
+    inst = build_instance(cfg)
+    p = params_for(cfg, chunk_rows=chunk)
+    log(f"pg_loss {cfg.name} N={inst['st'].N} chunk_rows={chunk}")
+    gpu = run_gpu(inst, p)
+    ref = run_oracle(inst, p)
+    compare_full(inst, gpu, ref, p, tag="seq")
+
+
+def test_pg_loss_token_mean_and_override():
+    cfg = WL.scaled_config("qwen8b_bf16")
+    inst = build_instance(cfg)
+    for kw in (dict(agg=rlk.AGG_TOKEN), dict(agg=rlk.AGG_SEQ, norm_override=5.0),
+               dict(agg=rlk.AGG_TOKEN, norm_override=1234.0, entropy_coef=0.01)):
+        p = params_for(cfg, chunk_rows=512, **kw)
+        compare_full(inst, run_gpu(inst, p), run_oracle(inst, p), p, tag=str(kw))
+
+
+def test_microbatch_accumulation_matches_one_call():
+    """Per-group calls with accumulate_dW and norm_override = Q add up to the one-call gradient."""
+    import torch
+
+    cfg = WL.scaled_config("small_bf16")
+    inst = build_instance(cfg)
+    st = inst["st"]
+    p = params_for(cfg)
+    full = run_gpu(inst, p)
+    Q = full["stats"]["n_groups"]
+    dW = torch.zeros_like(full["dW"])
+    tot = 0.0
+    for key in np.unique(st.group_ids):
+        rs = np.flatnonzero(st.group_ids == key)
+        rows = np.concatenate([np.arange(st.cu_seqlens[r], st.cu_seqlens[r + 1]) for r in rs])
+        lens = st.cu_seqlens[rs + 1] - st.cu_seqlens[rs]
+        rows_t = torch.as_tensor(rows, device="cuda")
+        sub = dict(inst)
+        sub.update(h=inst["h"][rows_t].contiguous(), targets=inst["targets"][rows_t].contiguous(),
+                   mask=inst["mask"][rows_t].contiguous(), old=inst["old"][rows_t].contiguous(),
+                   cu=_dev(np.concatenate([[0], np.cumsum(lens)]), torch.int32),
+                   rewards=_dev(st.rewards[rs], torch.float32), gid=_dev(st.group_ids[rs], torch.int32))
+        out = run_gpu(sub, params_for(cfg, accumulate_dW=True, norm_override=float(Q)), dW=dW)
+        tot += out["loss"]
+    err = rel_fro(to_host(dW), to_host(full["dW"]))
+    log(f"microbatch dW rel err {err:.3g}; loss {tot:.6g} vs {full['loss']:.6g}")
+    assert err <= 1e-3
+    assert abs(tot - full["loss"]) <= 1e-4 * max(1e-3, abs(full["loss"]))
+
+
+def test_determinism_and_masked_invariance():
+    import torch
+
+    cfg = WL.scaled_config("large_bf16")
+    inst = build_instance(cfg)
+    p = params_for(cfg, chunk_rows=256)
+    a = run_gpu(inst, p)
+    b = run_gpu(inst, p)
+    assert a["loss"] == b["loss"]
+    assert torch.equal(a["dh"], b["dh"]) and torch.equal(a["dW"], b["dW"])
+    # change every input on masked rows: outputs on trained rows are bitwise unchanged
+    st = inst["st"]
+    masked = torch.as_tensor(st.mask == 0, device="cuda")
+    pert = dict(inst)
+    h2 = inst["h"].clone()
+    h2[masked] = -3.0 * h2[masked]
+    t2 = inst["targets"].clone()
+    t2[masked] = 0
+    o2 = inst["old"].clone()
+    o2[masked] = 5.0
+    pert.update(h=h2, targets=t2, old=o2)
+    c = run_gpu(pert, p)
+    assert c["loss"] == a["loss"]
+    assert torch.equal(c["dW"], a["dW"]) and torch.equal(c["dh"], a["dh"])
+
+
+def test_empty_and_fully_excluded_batches():
+    import torch
+
+    cfg = WL.scaled_config("small_bf16")
+    inst = build_instance(cfg)
+    p = params_for(cfg)
+    dW0 = torch.full(inst["W"].shape, 7.0, dtype=torch.float32, device="cuda")
+    out = run_gpu(inst, p, mask=torch.zeros_like(inst["mask"]), dW=dW0)
+    assert out["loss"] == 0.0 and out["flags"] == 0
+    assert int(torch.count_nonzero(out["dh"])) == 0 and int(torch.count_nonzero(out["dW"])) == 0
+    assert out["stats"]["n_policy_tokens"] == 0
+    gid = torch.full_like(inst["gid"], -1)
+    out = run_gpu(inst, p, gid=gid)
+    assert out["loss"] == 0.0 and out["stats"]["n_groups"] == 0
+    assert int(torch.count_nonzero(out["dh"])) == 0 and int(torch.count_nonzero(out["dW"])) == 0
+
+
+def test_device_data_errors_are_flagged():
+    import torch
+
+    cfg = WL.scaled_config("small_bf16")
+    inst = build_instance(cfg)
+    p = params_for(cfg)
+    st = inst["st"]
+    t2 = inst["targets"].clone()
+    pol = int(np.flatnonzero(st.mask)[3])
+    t2[pol] = cfg.V + 5
+    bad = dict(inst)
+    bad["targets"] = t2
+    assert run_gpu(bad, p)["flags"] & rlk.DERR_TARGET
+    cu2 = inst["cu"].clone()
+    cu2[-1] = cu2[-1] - 3
+    bad = dict(inst)
+    bad["cu"] = cu2
+    assert run_gpu(bad, p)["flags"] & rlk.DERR_CU_SEQLENS
+    assert run_gpu(inst, p)["flags"] == 0
+
+
+# ------------------------------------------------------------------ full-size, sampled rows
+@pytest.mark.parametrize("name", ["small_bf16", "qwen8b_bf16"])
+def test_full_size_sampled_rows(name):
+    """Full-size batch in the configuration the benchmark times: integer outputs bit-exact,
+    per-token log-prob / entropy / lse and dhidden rows on seeded sampled rows, dW by the
+    zero column-sum property."""
+    import torch
+
+    cfg = WL.get_config(name)
+    inst = build_instance(cfg)
+    st = inst["st"]
+    p = params_for(cfg)
+    log(f"full-size {name} N={st.N}")
+    gpu = run_gpu(inst, p)
+    assert gpu["flags"] == 0
+    idx, tr, npol = O.compact(st.mask, st.cu_seqlens, st.group_ids)
+    ga = O.group_advantage(st.rewards, st.group_ids, p.adv_eps)
+    assert gpu["stats"]["n_policy_tokens"] == idx.shape[0] and gpu["stats"]["n_groups"] == ga["n_groups"]
+    omega = O.token_weights(tr, npol, ga["group_index"], ga["G"], ga["n_groups"], p.agg)
+    pick = np.sort(WL.sample_policy_rows(np.arange(idx.shape[0]), 192, seed=cfg.seed + 7))
+    rows = idx[pick]
+    rows_t = torch.as_tensor(rows, device="cuda")
+    ref = O.sampled_rows(to_host(inst["h"][rows_t]), to_host(inst["W"]), st.targets[rows], inst["old_host"][rows],
+                         ga["adv"][tr[pick]], omega[pick], eps_low=p.eps_low, eps_high=p.eps_high,
+                         entropy_coef=p.entropy_coef)
+    lp = gpu["logp"][rows_t].cpu().numpy()
+    en = gpu["ent"][rows_t].cpu().numpy()
+    dh = to_host(gpu["dh"][rows_t])
+    e_lp, e_en = np.abs(lp - ref["logp"]).max(), np.abs(en - ref["H"]).max()
+    e_dh = rel_fro(dh, ref["dh"])
+    colsum = to_host(gpu["dW"].sum(dim=0))
+    rel_cs = float(np.abs(colsum).max() / max(1e-30, float(gpu["dW"].abs().sum(dim=0).max())))
+    log(f"  sampled: logp {e_lp:.3g} ent {e_en:.3g} dh {e_dh:.3g}; dW colsum rel {rel_cs:.3g}")
+    tol = TOL_LOGP[cfg.dtype]
+    assert e_lp <= tol and e_en <= tol and e_dh <= TOL_GRAD
+    assert rel_cs <= 1e-2
+    assert np.isfinite(gpu["loss"])

@@ -115,9 +115,9 @@ def get_config(name: str) -> Config:
 _SCALED = {
     "tiny_fp32": dict(),
     "small_bf16": dict(groups=2, rollouts_per_group=4, len_min=640, len_max=640),
-    "qwen8b_bf16": dict(groups=2, rollouts_per_group=4, len_min=400, len_max=400),
-    "long_bf16": dict(groups=2, rollouts_per_group=3, len_min=520, len_max=900, tool_mean=48.0),
-    "large_bf16": dict(groups=3, rollouts_per_group=4, len_min=128, len_max=400,
+    "qwen8b_bf16": dict(groups=2, rollouts_per_group=4, len_min=240, len_max=240),
+    "long_bf16": dict(groups=2, rollouts_per_group=3, len_min=300, len_max=520, tool_mean=48.0),
+    "large_bf16": dict(groups=3, rollouts_per_group=4, len_min=100, len_max=240,
                        forced_equal_groups=(0.625,)),
 }
 
