@@ -1,0 +1,236 @@
+"""Benchmark of the policy-gradient hot path on one MI355X.
+
+A step is one pass of the whole path over one synthetic agentic-RL batch already resident
+in HBM: rlk_group_advantage + rlk_pg_loss_fwd_bwd (compaction, advantages, LM-head GEMM with
+online log-softmax, loss, dz, dhidden and dW GEMMs).  Prints one JSON line.
+
+  python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload qwen8b_bf16]
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+PEAK_BF16 = 2.5e15      # MI355X dense bf16 MFMA, FLOP/s
+PEAK_FP32_MFMA = 157.3e12
+PEAK_HBM = 8.0e12       # B/s
+METRIC = "policy tokens/sec for logprob+PG loss fwd+bwd; % of bf16 MFMA peak"
+GEMM_KINDS = ("fwd_lse_gemm", "dh_gemm", "dw_gemm")
+PROFILES = os.path.join(ROOT, "profiles")
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def build_inputs(cfg, device="cuda"):
+    import numpy as np
+    import torch
+
+    import workloads as WL
+    from workloads.anchor import gaussian_anchor
+
+    st = WL.make_structure(cfg)
+    h, W = WL.make_tensors(cfg, st.N, device=device)
+    anchor = gaussian_anchor(h, W, st.targets, cfg.w_std)
+    old = WL.old_logp_from_anchor(anchor, st)
+    dev = lambda a, dt: torch.as_tensor(np.asarray(a), dtype=dt, device=device)
+    return dict(st=st, h=h, W=W, cu=dev(st.cu_seqlens, torch.int32), mask=dev(st.mask, torch.uint8),
+                targets=dev(st.targets, torch.int32), rewards=dev(st.rewards, torch.float32),
+                gid=dev(st.group_ids, torch.int32), old=dev(old, torch.float32), old_host=old)
+
+
+def kernel_source_digest() -> str:
+    d = os.path.join(ROOT, "paper_2608_16798_amd", "csrc")
+    h = hashlib.sha256()
+    for f in sorted(os.listdir(d)):
+        if f.endswith((".hip", ".h")):
+            h.update(open(os.path.join(d, f), "rb").read())
+    return h.hexdigest()[:16]
+
+
+def read_traffic(kernel: str, workload: str, digest: str):
+    """HBM bytes per launch of `kernel` from the committed rocprofv3 counter summary, if it was
+    taken from the current kernel sources (else None)."""
+    path = os.path.join(PROFILES, f"{kernel}_{workload}_traffic.txt")
+    if not os.path.exists(path):
+        return None
+    kv = {}
+    for line in open(path):
+        if ":" in line and not line.startswith("#"):
+            k, v = line.split(":", 1)
+            kv[k.strip()] = v.strip()
+    if kv.get("kernel_source_digest") != digest:
+        return None
+    try:
+        return float(kv["hbm_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
+
+
+def cpu_baseline(cfg, inp, target_tokens: int):
+    """The fp64 oracle, as it stands, on the first rollouts of the same batch (>= target_tokens
+    policy tokens): forward, loss terms, dhidden rows and their dW contribution."""
+    import numpy as np
+
+    import oracle as O
+
+    st = inp["st"]
+    cu = st.cu_seqlens
+    keep_rollouts = 0
+    n = 0
+    while keep_rollouts < st.R and n < target_tokens:
+        r = keep_rollouts
+        n += int(st.mask[cu[r]:cu[r + 1]].sum())
+        keep_rollouts += 1
+    Nt = int(cu[keep_rollouts])
+    h = inp["h"][:Nt].float().cpu().numpy()
+    W = inp["W"].float().cpu().numpy()
+    threads = None
+    try:
+        from threadpoolctl import threadpool_info
+
+        threads = max((i.get("num_threads") or 0) for i in threadpool_info()) or None
+    except Exception:
+        pass
+    t0 = time.perf_counter()
+    out = O.pg_loss_fwd_bwd(h, W, st.targets[:Nt], st.mask[:Nt], cu[:keep_rollouts + 1], inp["old_host"][:Nt],
+                            st.rewards[:keep_rollouts], st.group_ids[:keep_rollouts], eps_low=cfg.eps_low,
+                            eps_high=cfg.eps_high, entropy_coef=cfg.entropy_coef)
+    dt = time.perf_counter() - t0
+    ntok = out["stats"]["n_policy_tokens"]
+    return {"value": ntok / dt, "unit": "policy tokens/s", "cores": threads or os.cpu_count(), "kind": "oracle",
+            "sample": f"first {keep_rollouts} rollouts ({ntok} policy tokens, full V={cfg.V}, d={cfg.d}, "
+                      f"fwd+loss+dhidden+dW contribution), fp64 NumPy, {dt:.1f} s",
+            "seconds": dt}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--workload", default="qwen8b_bf16")
+    ap.add_argument("--chunk-rows", type=int, default=0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-tokens", type=int, default=1024)
+    ap.add_argument("--no-kernel-events", action="store_true",
+                    help="time the steps without per-kernel HIP events (roofline then null)")
+    args = ap.parse_args()
+
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only: this build has no multi-GPU path (--gpus {args.gpus} requested)",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import paper_2608_16798_amd as rlk
+    import workloads as WL
+
+    if not os.path.exists(rlk.LIB_PATH):
+        from paper_2608_16798_amd.build import build
+
+        build(verbose=False)
+    rlk.load_library()
+    if not torch.cuda.is_available():
+        raise SystemExit("bench.py needs a GPU")
+    torch.cuda.set_device(0)
+
+    cfg = WL.get_config(args.workload)
+    log(f"[bench] building {cfg.name} inputs")
+    inp = build_inputs(cfg)
+    st = inp["st"]
+    N, R = st.N, st.R
+    dev = "cuda"
+    params = rlk.make_params(eps_low=cfg.eps_low, eps_high=cfg.eps_high, entropy_coef=cfg.entropy_coef,
+                             chunk_rows=args.chunk_rows)
+    batch = rlk.make_batch(inp["h"], inp["W"], inp["cu"])
+    ws = rlk.alloc_workspace(rlk.workspace_size(batch, params), dev)
+    ws_adv = rlk.alloc_workspace(rlk.advantage_workspace_size(R), dev)
+    adv = torch.empty(R, dtype=torch.float32, device=dev)
+    loss = torch.empty(1, dtype=torch.float32, device=dev)
+    dh = torch.empty_like(inp["h"])
+    dW = torch.empty(inp["W"].shape, dtype=torch.float32, device=dev)
+    stats = rlk.stats_buffer(dev)
+    stream = torch.cuda.current_stream()
+
+    def step():
+        rlk.group_advantage(inp["rewards"], inp["gid"], params.adv_eps, adv=adv, ws=ws_adv, stream=stream)
+        rlk.pg_loss_fwd_bwd(inp["h"], inp["W"], inp["targets"], inp["mask"], inp["cu"], inp["old"], inp["rewards"],
+                            inp["gid"], params, loss=loss, dhidden=dh, dW=dW, stats=stats, ws=ws, stream=stream)
+
+    log(f"[bench] warmup {args.warmup} step(s), N={N} R={R} ws={ws.numel() / 2**30:.1f} GiB")
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    if rlk.check_status(ws) != 0:
+        raise SystemExit("device data error in the benchmark batch")
+    s = rlk.stats_from_tensor(stats)
+    n_eff = int(s["n_policy_tokens"])
+
+    log(f"[bench] timing {args.steps} step(s)")
+    use_events = not args.no_kernel_events
+    torch.cuda.synchronize()
+    if use_events:
+        rlk.profile_begin()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    kern = rlk.profile_end() if use_events else {}
+    ms_per_step = (t1 - t0) * 1e3 / args.steps
+    value = n_eff / (ms_per_step / 1e3)
+    alg_flops = 6.0 * n_eff * cfg.V * cfg.d
+    peak = PEAK_BF16 if cfg.dtype == "bf16" else PEAK_FP32_MFMA
+    mfma_frac = alg_flops / (ms_per_step / 1e3) / peak
+    log(f"[bench] {ms_per_step:.2f} ms/step, {value:.0f} policy tokens/s, {100 * mfma_frac:.1f}% of MFMA peak")
+
+    roofline = None
+    per_kernel = {}
+    if kern:
+        for k, (ms, cnt) in sorted(kern.items(), key=lambda kv: -kv[1][0]):
+            per_kernel[k] = {"ms_per_step": round(ms / args.steps, 4), "launches_per_step": cnt // args.steps}
+        dom = max(GEMM_KINDS, key=lambda k: kern.get(k, (0.0, 1))[0])
+        ms, cnt = kern[dom]
+        avg_ms = ms / cnt
+        flops_per_launch = 2.0 * n_eff * cfg.V * cfg.d * args.steps / cnt
+        achieved = flops_per_launch / (avg_ms / 1e3) / 1e12
+        digest = kernel_source_digest()
+        traffic = read_traffic(dom, cfg.name, digest)
+        roofline = {"kernel": dom, "bound": "mfma", "achieved": round(achieved, 1), "peak": peak / 1e12,
+                    "unit": "TFLOP/s", "frac": round(achieved * 1e12 / peak, 4), "traffic": traffic,
+                    "avg_launch_ms": round(avg_ms, 3), "launches": cnt,
+                    "flops_per_launch": flops_per_launch, "kernel_source_digest": digest}
+        log("[bench] per-kernel ms/step: " + ", ".join(f"{k}={v['ms_per_step']}" for k, v in per_kernel.items()))
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        log(f"[bench] timing the fp64 oracle on >= {args.cpu_tokens} policy tokens")
+        cpu = cpu_baseline(cfg, inp, args.cpu_tokens)
+        log(f"[bench] oracle {cpu['value']:.1f} policy tokens/s in {cpu['seconds']:.1f} s")
+
+    out = {
+        "metric": METRIC, "value": round(value, 1), "unit": "policy tokens/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(ms_per_step, 3), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": cfg.dtype, "data": "synthetic",
+        "config": dict(WL.configs.describe(cfg, N), N_eff=n_eff, chunk_rows=args.chunk_rows or "auto"),
+        "mfma_pct_of_peak": round(100 * mfma_frac, 2),
+        "roofline": roofline, "cpu_baseline": cpu, "kernels": per_kernel,
+    }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -7,11 +7,13 @@
 //
 // Tile geometry (gfx950): 256 x 256 output tile per workgroup of 4 wavefronts (2 x 2), each
 // wavefront owning 128 x 128 = 4 x 4 blocks of v_mfma_f32_32x32x16_bf16 (fp32 operands use
-// v_mfma_f32_32x32x2_f32).  A stage holds 128 bytes of K per row (64 bf16 / 32 fp32) for both
-// operands, staged through LDS with a 16-byte row pad (conflict-free 16-byte fragment
-// reads) and double-buffered: 2 x 2 x 36 KiB = 144 KiB of the 160 KiB LDS.  Each lane's
-// MFMA fragment carries 8 consecutive K elements of one row (16 bytes); A and B use the
-// same K assignment, so the lane split of K inside the MFMA is irrelevant to the sum.
+// v_mfma_f32_32x32x2_f32); the 256 accumulators per lane live in AGPRs.  Operands stream through
+// LDS in 64-byte K slices (32 bf16 / 16 fp32 per row) copied straight from global memory by
+// buffer_load ... lds (no staging registers), four slices in flight: 4 x 2 x 16 KiB = 128 KiB of
+// the 160 KiB LDS.  Rows are XOR-swizzled at 16-byte granularity so MFMA fragment reads are
+// bank-conflict free.  Each lane's MFMA fragment carries 8 consecutive K elements of one row
+// (16 bytes); A and B use the same K assignment, so the lane split of K inside the MFMA is
+// irrelevant to the sum.
 //
 // Output layout of a 32x32 MFMA block: lane l holds column (l % 32); accumulator register r
 // holds row 8*(r/4) + 4*(l/32) + (r%4).  With vocabulary on M and tokens on N, every lane's
@@ -30,15 +32,85 @@ namespace rlk {
 namespace {
 
 constexpr int NT = 256;
-constexpr int KB = 128;                 // bytes of K per stage per row
-constexpr int LROW = KB + 16;           // LDS row stride (bytes)
-constexpr int TILE_B = kTile * LROW;    // 36864
-constexpr int STAGE_B = 2 * TILE_B;     // A + B
-constexpr int LDS_B = 2 * STAGE_B;      // 147456
+#ifndef RLK_KS
+#define RLK_KS 128
+#endif
+#ifndef RLK_NSTAGE
+#define RLK_NSTAGE 2
+#endif
+constexpr int KS = RLK_KS;              // bytes of K per pipeline slice per row (64 or 128)
+constexpr int NSTAGE = RLK_NSTAGE;      // LDS buffers in the copy pipeline
+constexpr int CPR = KS / 16;            // 16-byte chunks per row of a slice
+constexpr int RPI = 64 / CPR;           // rows per LDS-DMA instruction
+constexpr int IPW = kTile / RPI / 4;    // LDS-DMA instructions per wavefront per operand
+constexpr int NKK = KS / 32;            // MFMA K steps per slice
+constexpr int DMA_PER_SLICE = 2 * IPW;  // vector-memory instructions per wavefront per slice
+constexpr int OPND_B = kTile * KS;      // one operand's slice
+constexpr int STAGE_B = 2 * OPND_B;     // A + B
+constexpr int PIPE_B = NSTAGE * STAGE_B;
+static_assert(PIPE_B <= 131072 && (KS == 64 || KS == 128), "pipeline geometry");
 constexpr int QROW = kTile * 2 + 16;    // LDS row stride of the bf16 probability tile (bytes)
 constexpr int RED_OFF = kTile * QROW;   // 135168: reduction scratch after the staged tile
-constexpr int GROUP_M = 8;
+constexpr int LDS_B = RED_OFF + 3 * 2 * kTile * 4;  // 141312 >= PIPE_B
+constexpr int GROUP_M = 16;
 constexpr float kLog2e = 1.4426950408889634f;
+constexpr int kBufferFlags = 0x00020000;  // raw buffer: 32-bit data format, offset range-checked
+
+// Scheduling hints: interleave LDS fragment reads / global loads with the MFMA chain.
+#define SCHED_INTERLEAVE_DS(n)                                            \
+  do {                                                                   \
+    _Pragma("unroll") for (int _i = 0; _i < (n); ++_i) {                 \
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0); /* MFMA */      \
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0); /* DS read */   \
+    }                                                                    \
+    __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);                   \
+  } while (0)
+#define SCHED_INTERLEAVE_VMEM_DS()                                        \
+  do {                                                                   \
+    _Pragma("unroll") for (int _i = 0; _i < 8; ++_i) {                   \
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                 \
+      __builtin_amdgcn_sched_group_barrier(0x020, 2, 0); /* VMEM read */ \
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);                 \
+    }                                                                    \
+    __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);                   \
+  } while (0)
+
+
+#define LDSP(p) ((__attribute__((address_space(3))) void*)(p))
+
+// 16-byte-chunk XOR swizzle of an LDS row (CPR chunks): fragment reads of 8 or 16 consecutive
+// rows at one logical chunk touch distinct banks (for 32 and for 64 four-byte banks).
+__device__ __forceinline__ int swz(int r) {
+  if constexpr (CPR == 8) return (r ^ (r >> 3)) & 7;
+  else return ((r >> 1) ^ (r >> 3)) & 3;
+}
+
+// s_waitcnt with only the vector-memory counter constrained (gfx9 encoding: vmcnt[3:0] in
+// bits 3:0, vmcnt[5:4] in bits 15:14, expcnt 7 and lgkmcnt 15 = no wait).
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
+}
+__device__ __forceinline__ void wait_vmcnt_dyn(int n) {
+  if (n >= 48) wait_vmcnt<48>();
+  else if (n >= 32) wait_vmcnt<32>();
+  else if (n >= 24) wait_vmcnt<24>();
+  else if (n >= 16) wait_vmcnt<16>();
+  else if (n >= 8) wait_vmcnt<8>();
+  else wait_vmcnt<0>();
+}
+// LDS/scalar counter to zero, vector memory unconstrained.
+__device__ __forceinline__ void wait_lgkm0() { __builtin_amdgcn_s_waitcnt(0xC07F); }
+
+// Workgroup barrier without a memory fence: the copies still in flight must stay in flight, so
+// the waits are explicit (above); the empty asm statements keep the compiler from moving memory
+// accesses across the barrier.
+__device__ __forceinline__ void block_barrier() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
 
 enum { EPI_FWD = 0, EPI_DH = 1, EPI_DW = 2 };
 
@@ -81,26 +153,34 @@ __device__ __forceinline__ void store_elem<float>(float* p, float x) { *p = x; }
 template <>
 __device__ __forceinline__ void store_elem<bf16_t>(bf16_t* p, float x) { p->bits = bf16_bits(x); }
 
-// XCD-aware, L2-grouped tile mapping.  Returns false for workgroups beyond the tile grid.
+// XCD-aware tile mapping.  Workgroup ids are dispatched round-robin over the 8 XCDs, so the 256
+// workgroups resident at a time are 256 consecutive ids.  Tiles are rastered in column groups of
+// GROUP_M = 16 M-tiles, so 256 consecutive raster positions cover a 16 x 16 block of tiles; within
+// each aligned run of 256 ids the ids are permuted so that XCD x computes the 4 x 8 sub-block
+// (M-tiles 4 (x % 4) .. + 4, N-tiles 8 (x / 4) .. + 8) of that block: its 32 CUs then share 4 A
+// and 8 B panels in the XCD's L2, and each panel is shared by 2 (A) or 4 (B) XCDs through the
+// memory-side cache.  Returns false for workgroups beyond the tile grid.
 __device__ __forceinline__ bool map_tile(int tm, int tn, int& tile_m, int& tile_n) {
   const int total = tm * tn;
   const int pid = blockIdx.x;
   if (pid >= total) return false;
-  const int xcd = pid & 7, local = pid >> 3;
-  const int base = total >> 3, rem = total & 7;
-  const int start = xcd < rem ? xcd * (base + 1) : rem * (base + 1) + (xcd - rem) * base;
-  const int npid = start + local;
+  int idx = pid;
+  if ((pid | 255) < total) {  // a complete run of 256 ids: XCD-blocked permutation
+    const int xcd = pid & 7, slot = (pid >> 3) & 31;
+    const int m = 4 * (xcd & 3) + (slot & 3), n = 8 * (xcd >> 2) + (slot >> 2);
+    idx = (pid & ~255) + n * 16 + m;
+  }
   const int group_sz = GROUP_M * tn;
-  const int g = npid / group_sz;
+  const int g = idx / group_sz;
   const int first_m = g * GROUP_M;
   const int gm = min(tm - first_m, GROUP_M);
-  const int in = npid - g * group_sz;
+  const int in = idx - g * group_sz;
   tile_m = first_m + in % gm;
   tile_n = in / gm;
   return true;
 }
 
-template <typename T, int EPI, bool STORE_Q>
+template <typename T, int EPI, bool STORE_Q, bool KTAIL>
 __global__ void __launch_bounds__(NT, 1) k_gemm(GemmArgs a) {
   __shared__ __attribute__((aligned(16))) char smem[LDS_B];
 
@@ -122,43 +202,64 @@ __global__ void __launch_bounds__(NT, 1) k_gemm(GemmArgs a) {
   const int lane = tid & 63, wid = tid >> 6, wm = wid >> 1, wn = wid & 1;
   const int lrow = lane & 31, lh = lane >> 5;
 
-  // ---- operand row pointers for the global->LDS copy: rows (tid>>3) + 32 i, 16-byte column tid&7
-  const int64_t lda_b = a.lda * (int64_t)sizeof(T), ldb_b = a.ldb * (int64_t)sizeof(T);
-  const char* pa[8];
-  const char* pb[8];
-#pragma unroll
-  for (int i = 0; i < 8; ++i) {
-    int ra = min(tile_m * kTile + (tid >> 3) + 32 * i, M - 1);
-    int rb = min(tile_n * kTile + (tid >> 3) + 32 * i, N - 1);
-    pa[i] = reinterpret_cast<const char*>(a.A) + (int64_t)ra * lda_b + (tid & 7) * 16;
-    pb[i] = reinterpret_cast<const char*>(a.B) + (int64_t)rb * ldb_b + (tid & 7) * 16;
-  }
+  // ---- operand panels as buffer resources: rows beyond M/N (and, with KTAIL, K chunks beyond K)
+  // read as zero through the hardware range check; 32-bit offsets address one 256-row panel.
+  const uint32_t lda_b = (uint32_t)(a.lda * (int64_t)sizeof(T)), ldb_b = (uint32_t)(a.ldb * (int64_t)sizeof(T));
+  const int rows_a = min(kTile, M - tile_m * kTile), rows_b = min(kTile, N - tile_n * kTile);
+  const __amdgpu_buffer_rsrc_t rsa = __builtin_amdgcn_make_buffer_rsrc(
+      (void*)(reinterpret_cast<const char*>(a.A) + (int64_t)tile_m * kTile * lda_b), (short)0,
+      (int)((uint32_t)rows_a * lda_b), kBufferFlags);
+  const __amdgpu_buffer_rsrc_t rsb = __builtin_amdgcn_make_buffer_rsrc(
+      (void*)(reinterpret_cast<const char*>(a.B) + (int64_t)tile_n * kTile * ldb_b), (short)0,
+      (int)((uint32_t)rows_b * ldb_b), kBufferFlags);
   const int64_t Kb = (int64_t)K * sizeof(T);
-  const int nk = (int)((Kb + KB - 1) / KB);
+  const int nk = (int)((Kb + KS - 1) / KS);
 
-  u32x4 ra[8], rb[8];
-  auto gload = [&](int kt) {
-    const int64_t kb = (int64_t)kt * KB;
-    const bool ok = kb + (tid & 7) * 16 < Kb;
+  // Direct global->LDS copies (LDS DMA): one instruction moves 64 lanes x 16 bytes into 1 KiB of
+  // LDS at consecutive addresses, i.e. RPI rows of one K slice.  Wave w fills rows
+  // [w * IPW * RPI, (w + 1) * IPW * RPI) of each operand with IPW instructions; lane l of
+  // instruction j carries row (w * IPW + j) * RPI + l / CPR into LDS slot l % CPR, which holds the
+  // logical 16-byte K chunk (l % CPR) ^ swz(row).
+  uint32_t voa[IPW], vob[IPW];
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      if (ok) {
-        ra[i] = *reinterpret_cast<const u32x4*>(pa[i] + kb);
-        rb[i] = *reinterpret_cast<const u32x4*>(pb[i] + kb);
-      } else {
-        ra[i] = u32x4{0, 0, 0, 0};
-        rb[i] = u32x4{0, 0, 0, 0};
+  for (int j = 0; j < IPW; ++j) {
+    const int row = (wid * IPW + j) * RPI + lane / CPR;
+    const int chunk = (lane % CPR) ^ swz(row);
+    voa[j] = (uint32_t)row * lda_b + chunk * 16;
+    vob[j] = (uint32_t)row * ldb_b + chunk * 16;
+  }
+  auto dma = [&](int kt) {
+    char* st = smem + (kt % NSTAGE) * STAGE_B;
+    const uint32_t kb = (uint32_t)kt * KS;
+#pragma unroll
+    for (int j = 0; j < IPW; ++j) {
+      uint32_t oa = voa[j], ob = vob[j];
+      if constexpr (KTAIL) {
+        // chunks past the end of K would read the next row: push them out of range (zero fill)
+        const int row = (wid * IPW + j) * RPI + lane / CPR;
+        const uint32_t ck = kb + (((lane % CPR) ^ swz(row)) * 16);
+        if ((int64_t)ck >= Kb) {
+          oa = 0x80000000u;
+          ob = 0x80000000u;
+        }
       }
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rsa, LDSP(st + (wid * IPW + j) * 1024), 16, oa, kb, 0, 0);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rsb, LDSP(st + OPND_B + (wid * IPW + j) * 1024), 16, ob, kb, 0, 0);
     }
   };
-  auto sstore = [&](int buf) {
-    char* sA = smem + buf * STAGE_B;
-    char* sB = sA + TILE_B;
+  // Fragment reads: lane (lrow, lh) takes logical K chunk 2 kk + lh of row r.
+  auto frags = [&](int kt, int kk, u32x4 (&fa)[4], u32x4 (&fb)[4]) {
+    const char* sA = smem + (kt % NSTAGE) * STAGE_B;
+    const char* sB = sA + OPND_B;
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      const int off = ((tid >> 3) + 32 * i) * LROW + (tid & 7) * 16;
-      *reinterpret_cast<u32x4*>(sA + off) = ra[i];
-      *reinterpret_cast<u32x4*>(sB + off) = rb[i];
+    for (int mb = 0; mb < 4; ++mb) {
+      const int r = wm * 128 + mb * 32 + lrow;
+      fa[mb] = *reinterpret_cast<const u32x4*>(sA + r * KS + (((2 * kk + lh) ^ swz(r)) * 16));
+    }
+#pragma unroll
+    for (int nb = 0; nb < 4; ++nb) {
+      const int r = wn * 128 + nb * 32 + lrow;
+      fb[nb] = *reinterpret_cast<const u32x4*>(sB + r * KS + (((2 * kk + lh) ^ swz(r)) * 16));
     }
   };
 
@@ -169,31 +270,72 @@ __global__ void __launch_bounds__(NT, 1) k_gemm(GemmArgs a) {
     for (int j = 0; j < 4; ++j)
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
+  auto mma16 = [&](const u32x4 (&fa)[4], const u32x4 (&fb)[4]) {
+#pragma unroll
+    for (int mb = 0; mb < 4; ++mb)
+#pragma unroll
+      for (int nb = 0; nb < 4; ++nb) Op<T>::mma(acc[mb][nb], fa[mb], fb[nb]);
+  };
 
-  gload(0);
-  sstore(0);
-  __syncthreads();
-  for (int kt = 0; kt < nk; ++kt) {
-    if (kt + 1 < nk) gload(kt + 1);
-    const char* sA = smem + (kt & 1) * STAGE_B;
-    const char* sB = sA + TILE_B;
-#pragma unroll
-    for (int kk = 0; kk < 4; ++kk) {
-      u32x4 af[4], bfr[4];
-#pragma unroll
-      for (int mb = 0; mb < 4; ++mb)
-        af[mb] = *reinterpret_cast<const u32x4*>(sA + (wm * 128 + mb * 32 + lrow) * LROW + kk * 32 + lh * 16);
-#pragma unroll
-      for (int nb = 0; nb < 4; ++nb)
-        bfr[nb] = *reinterpret_cast<const u32x4*>(sB + (wn * 128 + nb * 32 + lrow) * LROW + kk * 32 + lh * 16);
-#pragma unroll
-      for (int mb = 0; mb < 4; ++mb)
-#pragma unroll
-        for (int nb = 0; nb < 4; ++nb) Op<T>::mma(acc[mb][nb], af[mb], bfr[nb]);
-    }
-    if (kt + 1 < nk) sstore((kt + 1) & 1);
-    __syncthreads();
+  // Pipeline over K slices with NSTAGE LDS buffers: the copy of slice kt + NSTAGE is issued
+  // right after the barrier that retires slice kt, so every copy has NSTAGE - 1 slices of MFMA
+  // work to land.  Within a slice, the fragments of K step kk + 1 are read under the 16 MFMAs of
+  // step kk; at the last step this wave's copies of slice kt + 1 are awaited, one barrier
+  // publishes every wave's copies (and retires slice kt), slice kt + NSTAGE is issued into the
+  // freed buffer and the first fragments of slice kt + 1 are read.
+  u32x4 f0a[4], f0b[4], f1a[4], f1b[4];
+  const int npro = min(nk, NSTAGE);
+  for (int s = 0; s < npro; ++s) dma(s);
+  if (nk > 0) {
+    wait_vmcnt_dyn(DMA_PER_SLICE * (npro - 1));
+    block_barrier();
+    frags(0, 0, f0a, f0b);
   }
+  int kt = 0;
+  for (; kt + NSTAGE < nk; ++kt) {
+#pragma unroll
+    for (int kk = 0; kk < NKK; ++kk) {
+      u32x4(&ca)[4] = (kk & 1) ? f1a : f0a;
+      u32x4(&cb)[4] = (kk & 1) ? f1b : f0b;
+      u32x4(&na)[4] = (kk & 1) ? f0a : f1a;
+      u32x4(&nb)[4] = (kk & 1) ? f0b : f1b;
+      if (kk + 1 < NKK) {
+        frags(kt, kk + 1, na, nb);
+        mma16(ca, cb);
+        SCHED_INTERLEAVE_DS(8);
+      } else {
+        wait_vmcnt<DMA_PER_SLICE * (NSTAGE - 2)>();  // slice kt+1 has landed
+        wait_lgkm0();
+        block_barrier();
+        dma(kt + NSTAGE);
+        frags(kt + 1, 0, na, nb);
+        mma16(ca, cb);
+        SCHED_INTERLEAVE_VMEM_DS();
+      }
+    }
+  }
+  for (; kt < nk; ++kt) {
+    // drain: no refills
+#pragma unroll
+    for (int kk = 0; kk < NKK; ++kk) {
+      u32x4(&ca)[4] = (kk & 1) ? f1a : f0a;
+      u32x4(&cb)[4] = (kk & 1) ? f1b : f0b;
+      u32x4(&na)[4] = (kk & 1) ? f0a : f1a;
+      u32x4(&nb)[4] = (kk & 1) ? f0b : f1b;
+      if (kk + 1 < NKK) {
+        frags(kt, kk + 1, na, nb);
+      } else if (kt + 1 < nk) {
+        wait_vmcnt_dyn(DMA_PER_SLICE * min(nk - 2 - kt, NSTAGE - 2));
+        wait_lgkm0();
+        block_barrier();
+        frags(kt + 1, 0, na, nb);
+      }
+      mma16(ca, cb);
+    }
+  }
+  // the epilogues reuse the LDS of the pipeline
+  wait_lgkm0();
+  block_barrier();
 
   // ------------------------------------------------------------------ epilogues
   if constexpr (EPI == EPI_FWD) {
@@ -359,10 +501,14 @@ inline unsigned tiles(int64_t n) { return (unsigned)((n + kTile - 1) / kTile); }
 template <typename T>
 hipError_t fwd_impl(const GemmArgs& a, bool store_q, hipStream_t s) {
   dim3 grid(tiles(a.M) * tiles(a.Mc));
-  if (store_q)
-    k_gemm<T, EPI_FWD, true><<<grid, NT, 0, s>>>(a);
-  else
-    k_gemm<T, EPI_FWD, false><<<grid, NT, 0, s>>>(a);
+  const bool ktail = ((int64_t)a.K * (int64_t)sizeof(T)) % KS != 0;
+  if (store_q) {
+    if (ktail) k_gemm<T, EPI_FWD, true, true><<<grid, NT, 0, s>>>(a);
+    else k_gemm<T, EPI_FWD, true, false><<<grid, NT, 0, s>>>(a);
+  } else {
+    if (ktail) k_gemm<T, EPI_FWD, false, true><<<grid, NT, 0, s>>>(a);
+    else k_gemm<T, EPI_FWD, false, false><<<grid, NT, 0, s>>>(a);
+  }
   return hipGetLastError();
 }
 
@@ -379,9 +525,9 @@ hipError_t launch_dh_gemm(int dtype, const GemmArgs& a, hipStream_t s) {
   dim3 grid(tiles(a.Mc) * tiles(a.N));
   prof_mark(KK_DH_GEMM, true, s);
   if (dtype == RLK_DTYPE_BF16)
-    k_gemm<bf16_t, EPI_DH, false><<<grid, NT, 0, s>>>(a);
+    k_gemm<bf16_t, EPI_DH, false, false><<<grid, NT, 0, s>>>(a);
   else
-    k_gemm<float, EPI_DH, false><<<grid, NT, 0, s>>>(a);
+    k_gemm<float, EPI_DH, false, false><<<grid, NT, 0, s>>>(a);
   prof_mark(KK_DH_GEMM, false, s);
   return hipGetLastError();
 }
@@ -390,9 +536,9 @@ hipError_t launch_dw_gemm(int dtype, const GemmArgs& a, hipStream_t s) {
   dim3 grid(tiles(a.M) * tiles(a.N));
   prof_mark(KK_DW_GEMM, true, s);
   if (dtype == RLK_DTYPE_BF16)
-    k_gemm<bf16_t, EPI_DW, false><<<grid, NT, 0, s>>>(a);
+    k_gemm<bf16_t, EPI_DW, false, false><<<grid, NT, 0, s>>>(a);
   else
-    k_gemm<float, EPI_DW, false><<<grid, NT, 0, s>>>(a);
+    k_gemm<float, EPI_DW, false, false><<<grid, NT, 0, s>>>(a);
   prof_mark(KK_DW_GEMM, false, s);
   return hipGetLastError();
 }
