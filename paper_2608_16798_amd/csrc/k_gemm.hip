@@ -5,78 +5,77 @@
 //   dhidden : A = dz [tokens, Vp],   B = W^T [d, Vp]                   -> scatter to dh[idx]
 //   dW      : A = dz^T [Vp, tokens], B = hidden^T [d, tokens]          -> fp32 dW (+)=
 //
-// Tile geometry (gfx950): 256 x 256 output tile per workgroup of 4 wavefronts (2 x 2), each
-// wavefront owning 128 x 128 = 4 x 4 blocks of v_mfma_f32_32x32x16_bf16 (fp32 operands use
-// v_mfma_f32_32x32x2_f32); the 256 accumulators per lane live in AGPRs.  Operands stream through
-// LDS in 64-byte K slices (32 bf16 / 16 fp32 per row) copied straight from global memory by
-// buffer_load ... lds (no staging registers), four slices in flight: 4 x 2 x 16 KiB = 128 KiB of
-// the 160 KiB LDS.  Rows are XOR-swizzled at 16-byte granularity so MFMA fragment reads are
-// bank-conflict free.  Each lane's MFMA fragment carries 8 consecutive K elements of one row
-// (16 bytes); A and B use the same K assignment, so the lane split of K inside the MFMA is
-// irrelevant to the sum.
+// Tile geometry (gfx950): a 256 x 256 output tile per workgroup of WAVES_M x WAVES_N wavefronts,
+// each owning a (256 / WAVES_M) x (256 / WAVES_N) block of 32 x 32 v_mfma_f32_32x32x16_bf16
+// tiles (fp32 operands use v_mfma_f32_32x32x2_f32), accumulators in AGPRs.  Operands stream
+// through LDS in K slices of KS bytes per row, copied straight from global memory by
+// buffer_load ... lds (no staging registers) into NSTAGE buffers; rows are XOR-swizzled at 16-byte
+// granularity so MFMA fragment reads are bank-conflict free.  Each lane's MFMA fragment carries 8
+// consecutive K elements of one row (16 bytes); A and B use the same K assignment, so the lane
+// split of K inside the MFMA is irrelevant to the sum.
 //
 // Output layout of a 32x32 MFMA block: lane l holds column (l % 32); accumulator register r
 // holds row 8*(r/4) + 4*(l/32) + (r%4).  With vocabulary on M and tokens on N, every lane's
 // accumulators belong to a single token, so the vocabulary reduction of the online
 // log-softmax is in-register, then one cross-half exchange, then one LDS exchange between
-// the two wavefronts of a column.
-//
-// Workgroup-to-tile mapping is XCD-aware: consecutive workgroup ids are dispatched round-robin
-// over the 8 XCDs, so ids are re-packed to give each XCD a contiguous range of tiles, which
-// is then rastered in groups of 8 M-tiles so that concurrently resident tiles share operand
-// panels in that XCD's L2.
+// the wavefronts of a column.
 #include "rlk_internal.h"
 
 namespace rlk {
 
 namespace {
 
-constexpr int NT = 256;
 #ifndef RLK_KS
 #define RLK_KS 128
 #endif
 #ifndef RLK_NSTAGE
 #define RLK_NSTAGE 2
 #endif
+#ifndef RLK_WAVES_N
+#define RLK_WAVES_N 4
+#endif
+constexpr int WAVES_M = 2;
+constexpr int WAVES_N = RLK_WAVES_N;    // 2: one wavefront per SIMD; 4: two per SIMD
+constexpr int NWAVE = WAVES_M * WAVES_N;
+constexpr int NT = 64 * NWAVE;
+constexpr int WTM = kTile / WAVES_M;    // rows of a wavefront's block
+constexpr int WTN = kTile / WAVES_N;    // columns of a wavefront's block
+constexpr int MBW = WTM / 32;           // 32x32 MFMA tiles per wavefront along M
+constexpr int NBW = WTN / 32;           // ... along N
 constexpr int KS = RLK_KS;              // bytes of K per pipeline slice per row (64 or 128)
 constexpr int NSTAGE = RLK_NSTAGE;      // LDS buffers in the copy pipeline
 constexpr int CPR = KS / 16;            // 16-byte chunks per row of a slice
 constexpr int RPI = 64 / CPR;           // rows per LDS-DMA instruction
-constexpr int IPW = kTile / RPI / 4;    // LDS-DMA instructions per wavefront per operand
+constexpr int IPW = kTile / RPI / NWAVE;  // LDS-DMA instructions per wavefront per operand
 constexpr int NKK = KS / 32;            // MFMA K steps per slice
 constexpr int DMA_PER_SLICE = 2 * IPW;  // vector-memory instructions per wavefront per slice
 constexpr int OPND_B = kTile * KS;      // one operand's slice
 constexpr int STAGE_B = 2 * OPND_B;     // A + B
 constexpr int PIPE_B = NSTAGE * STAGE_B;
-static_assert(PIPE_B <= 131072 && (KS == 64 || KS == 128), "pipeline geometry");
+static_assert(PIPE_B <= 131072 && (KS == 64 || KS == 128) && IPW >= 1, "pipeline geometry");
 constexpr int QROW = kTile * 2 + 16;    // LDS row stride of the bf16 probability tile (bytes)
 constexpr int RED_OFF = kTile * QROW;   // 135168: reduction scratch after the staged tile
-constexpr int LDS_B = RED_OFF + 3 * 2 * kTile * 4;  // 141312 >= PIPE_B
+constexpr int LDS_B = RED_OFF + 3 * WAVES_M * kTile * 4;  // >= PIPE_B
 constexpr int GROUP_M = 16;
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr int kBufferFlags = 0x00020000;  // raw buffer: 32-bit data format, offset range-checked
 
-// Scheduling hints: interleave LDS fragment reads / global loads with the MFMA chain.
-#define SCHED_INTERLEAVE_DS(n)                                            \
-  do {                                                                   \
-    _Pragma("unroll") for (int _i = 0; _i < (n); ++_i) {                 \
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0); /* MFMA */      \
-      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0); /* DS read */   \
-    }                                                                    \
-    __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);                   \
-  } while (0)
-#define SCHED_INTERLEAVE_VMEM_DS()                                        \
-  do {                                                                   \
-    _Pragma("unroll") for (int _i = 0; _i < 8; ++_i) {                   \
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                 \
-      __builtin_amdgcn_sched_group_barrier(0x020, 2, 0); /* VMEM read */ \
-      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);                 \
-    }                                                                    \
-    __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);                   \
-  } while (0)
-
-
 #define LDSP(p) ((__attribute__((address_space(3))) void*)(p))
+
+// Scheduling hints for one MFMA K step: interleave the LDS fragment reads (and the global->LDS
+// copies of the next slice) with the MFMA chain.
+template <int NMFMA, int NDS, int NVMEM>
+__device__ __forceinline__ void sched_step() {
+#pragma unroll
+  for (int i = 0; i < NMFMA; ++i) {
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
+    if constexpr (NVMEM > 0) {
+      if (i * NVMEM / NMFMA != (i + 1) * NVMEM / NMFMA) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
+      if ((i + 1) * NVMEM / NMFMA - i * NVMEM / NMFMA > 1) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
+    }
+    if (i < NDS) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // DS read
+  }
+}
 
 // 16-byte-chunk XOR swizzle of an LDS row (CPR chunks): fragment reads of 8 or 16 consecutive
 // rows at one logical chunk touch distinct banks (for 32 and for 64 four-byte banks).
@@ -98,6 +97,7 @@ __device__ __forceinline__ void wait_vmcnt_dyn(int n) {
   else if (n >= 24) wait_vmcnt<24>();
   else if (n >= 16) wait_vmcnt<16>();
   else if (n >= 8) wait_vmcnt<8>();
+  else if (n >= 4) wait_vmcnt<4>();
   else wait_vmcnt<0>();
 }
 // LDS/scalar counter to zero, vector memory unconstrained.
@@ -181,7 +181,7 @@ __device__ __forceinline__ bool map_tile(int tm, int tn, int& tile_m, int& tile_
 }
 
 template <typename T, int EPI, bool STORE_Q, bool KTAIL>
-__global__ void __launch_bounds__(NT, 1) k_gemm(GemmArgs a) {
+__global__ void __launch_bounds__(NT) k_gemm(GemmArgs a) {
   __shared__ __attribute__((aligned(16))) char smem[LDS_B];
 
   int M = a.M, N = a.N, K = a.K;
@@ -199,7 +199,7 @@ __global__ void __launch_bounds__(NT, 1) k_gemm(GemmArgs a) {
   if (!map_tile(tm, tn, tile_m, tile_n)) return;
 
   const int tid = threadIdx.x;
-  const int lane = tid & 63, wid = tid >> 6, wm = wid >> 1, wn = wid & 1;
+  const int lane = tid & 63, wid = tid >> 6, wm = wid / WAVES_N, wn = wid % WAVES_N;
   const int lrow = lane & 31, lh = lane >> 5;
 
   // ---- operand panels as buffer resources: rows beyond M/N (and, with KTAIL, K chunks beyond K)
@@ -248,42 +248,42 @@ __global__ void __launch_bounds__(NT, 1) k_gemm(GemmArgs a) {
     }
   };
   // Fragment reads: lane (lrow, lh) takes logical K chunk 2 kk + lh of row r.
-  auto frags = [&](int kt, int kk, u32x4 (&fa)[4], u32x4 (&fb)[4]) {
+  auto frags = [&](int kt, int kk, u32x4 (&fa)[MBW], u32x4 (&fb)[NBW]) {
     const char* sA = smem + (kt % NSTAGE) * STAGE_B;
     const char* sB = sA + OPND_B;
 #pragma unroll
-    for (int mb = 0; mb < 4; ++mb) {
-      const int r = wm * 128 + mb * 32 + lrow;
+    for (int mb = 0; mb < MBW; ++mb) {
+      const int r = wm * WTM + mb * 32 + lrow;
       fa[mb] = *reinterpret_cast<const u32x4*>(sA + r * KS + (((2 * kk + lh) ^ swz(r)) * 16));
     }
 #pragma unroll
-    for (int nb = 0; nb < 4; ++nb) {
-      const int r = wn * 128 + nb * 32 + lrow;
+    for (int nb = 0; nb < NBW; ++nb) {
+      const int r = wn * WTN + nb * 32 + lrow;
       fb[nb] = *reinterpret_cast<const u32x4*>(sB + r * KS + (((2 * kk + lh) ^ swz(r)) * 16));
     }
   };
 
-  f32x16 acc[4][4];
+  f32x16 acc[MBW][NBW];
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+  for (int i = 0; i < MBW; ++i)
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
+    for (int j = 0; j < NBW; ++j)
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
-  auto mma16 = [&](const u32x4 (&fa)[4], const u32x4 (&fb)[4]) {
+  auto mma = [&](const u32x4 (&fa)[MBW], const u32x4 (&fb)[NBW]) {
 #pragma unroll
-    for (int mb = 0; mb < 4; ++mb)
+    for (int mb = 0; mb < MBW; ++mb)
 #pragma unroll
-      for (int nb = 0; nb < 4; ++nb) Op<T>::mma(acc[mb][nb], fa[mb], fb[nb]);
+      for (int nb = 0; nb < NBW; ++nb) Op<T>::mma(acc[mb][nb], fa[mb], fb[nb]);
   };
 
   // Pipeline over K slices with NSTAGE LDS buffers: the copy of slice kt + NSTAGE is issued
   // right after the barrier that retires slice kt, so every copy has NSTAGE - 1 slices of MFMA
-  // work to land.  Within a slice, the fragments of K step kk + 1 are read under the 16 MFMAs of
+  // work to land.  Within a slice, the fragments of K step kk + 1 are read under the MFMAs of
   // step kk; at the last step this wave's copies of slice kt + 1 are awaited, one barrier
   // publishes every wave's copies (and retires slice kt), slice kt + NSTAGE is issued into the
   // freed buffer and the first fragments of slice kt + 1 are read.
-  u32x4 f0a[4], f0b[4], f1a[4], f1b[4];
+  u32x4 f0a[MBW], f0b[NBW], f1a[MBW], f1b[NBW];
   const int npro = min(nk, NSTAGE);
   for (int s = 0; s < npro; ++s) dma(s);
   if (nk > 0) {
@@ -295,22 +295,22 @@ __global__ void __launch_bounds__(NT, 1) k_gemm(GemmArgs a) {
   for (; kt + NSTAGE < nk; ++kt) {
 #pragma unroll
     for (int kk = 0; kk < NKK; ++kk) {
-      u32x4(&ca)[4] = (kk & 1) ? f1a : f0a;
-      u32x4(&cb)[4] = (kk & 1) ? f1b : f0b;
-      u32x4(&na)[4] = (kk & 1) ? f0a : f1a;
-      u32x4(&nb)[4] = (kk & 1) ? f0b : f1b;
+      u32x4(&ca)[MBW] = (kk & 1) ? f1a : f0a;
+      u32x4(&cb)[NBW] = (kk & 1) ? f1b : f0b;
+      u32x4(&na)[MBW] = (kk & 1) ? f0a : f1a;
+      u32x4(&nb)[NBW] = (kk & 1) ? f0b : f1b;
       if (kk + 1 < NKK) {
         frags(kt, kk + 1, na, nb);
-        mma16(ca, cb);
-        SCHED_INTERLEAVE_DS(8);
+        mma(ca, cb);
+        sched_step<MBW * NBW, MBW + NBW, 0>();
       } else {
         wait_vmcnt<DMA_PER_SLICE * (NSTAGE - 2)>();  // slice kt+1 has landed
         wait_lgkm0();
         block_barrier();
         dma(kt + NSTAGE);
         frags(kt + 1, 0, na, nb);
-        mma16(ca, cb);
-        SCHED_INTERLEAVE_VMEM_DS();
+        mma(ca, cb);
+        sched_step<MBW * NBW, MBW + NBW, DMA_PER_SLICE>();
       }
     }
   }
@@ -318,10 +318,10 @@ __global__ void __launch_bounds__(NT, 1) k_gemm(GemmArgs a) {
     // drain: no refills
 #pragma unroll
     for (int kk = 0; kk < NKK; ++kk) {
-      u32x4(&ca)[4] = (kk & 1) ? f1a : f0a;
-      u32x4(&cb)[4] = (kk & 1) ? f1b : f0b;
-      u32x4(&na)[4] = (kk & 1) ? f0a : f1a;
-      u32x4(&nb)[4] = (kk & 1) ? f0b : f1b;
+      u32x4(&ca)[MBW] = (kk & 1) ? f1a : f0a;
+      u32x4(&cb)[NBW] = (kk & 1) ? f1b : f0b;
+      u32x4(&na)[MBW] = (kk & 1) ? f0a : f1a;
+      u32x4(&nb)[NBW] = (kk & 1) ? f0b : f1b;
       if (kk + 1 < NKK) {
         frags(kt, kk + 1, na, nb);
       } else if (kt + 1 < nk) {
@@ -330,7 +330,7 @@ __global__ void __launch_bounds__(NT, 1) k_gemm(GemmArgs a) {
         block_barrier();
         frags(kt + 1, 0, na, nb);
       }
-      mma16(ca, cb);
+      mma(ca, cb);
     }
   }
   // the epilogues reuse the LDS of the pipeline
@@ -338,26 +338,28 @@ __global__ void __launch_bounds__(NT, 1) k_gemm(GemmArgs a) {
   block_barrier();
 
   // ------------------------------------------------------------------ epilogues
+  // Accumulator (mb, nb, r) of this lane sits at tile row wm*WTM + mb*32 + 8*(r/4) + 4*lh + r%4 and
+  // tile column wn*WTN + nb*32 + lrow.
   if constexpr (EPI == EPI_FWD) {
     // rows = vocabulary v = v0 + rl, columns = chunk-local token n.
     const int v0 = tile_m * kTile;
     const int V = a.V;
     const bool full_v = v0 + kTile <= V;
-    float* red_m = reinterpret_cast<float*>(smem + RED_OFF);  // [2][256]
-    float* red_s = red_m + 2 * kTile;                          // [2][256]
-    float* red_u = red_s + 2 * kTile;                          // [2][256]
+    float* red_m = reinterpret_cast<float*>(smem + RED_OFF);  // [WAVES_M][256]
+    float* red_s = red_m + WAVES_M * kTile;                    // [WAVES_M][256]
+    float* red_u = red_s + WAVES_M * kTile;                    // [WAVES_M][256]
 
     // phase 1: per-token max over this tile's 256 vocabulary rows; gather the target logit.
 #pragma unroll
-    for (int nb = 0; nb < 4; ++nb) {
-      const int cl = wn * 128 + nb * 32 + lrow;
+    for (int nb = 0; nb < NBW; ++nb) {
+      const int cl = wn * WTN + nb * 32 + lrow;
       const int n = tile_n * kTile + cl;
       float mx = -INFINITY;
 #pragma unroll
-      for (int mb = 0; mb < 4; ++mb)
+      for (int mb = 0; mb < MBW; ++mb)
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-          const int rl = wm * 128 + mb * 32 + (r >> 2) * 8 + lh * 4 + (r & 3);
+          const int rl = wm * WTM + mb * 32 + (r >> 2) * 8 + lh * 4 + (r & 3);
           const float z = (full_v || v0 + rl < V) ? acc[mb][nb][r] : -INFINITY;
           mx = fmaxf(mx, z);
         }
@@ -365,12 +367,12 @@ __global__ void __launch_bounds__(NT, 1) k_gemm(GemmArgs a) {
       if (lh == 0) red_m[wm * kTile + cl] = mx;
       if (n < N) {
         const int y = a.ytgt[a.c0 + n];
-        const int yl = y - v0 - wm * 128;
-        if (y >= 0 && y < V && yl >= 0 && yl < 128 && ((yl >> 2) & 1) == lh) {
+        const int yl = y - v0 - wm * WTM;
+        if (y >= 0 && y < V && yl >= 0 && yl < WTM && ((yl >> 2) & 1) == lh) {
           const int tmb = yl >> 5, tr = ((yl & 31) >> 3) * 4 + (yl & 3);
           float z = 0.0f;
 #pragma unroll
-          for (int mb = 0; mb < 4; ++mb)
+          for (int mb = 0; mb < MBW; ++mb)
 #pragma unroll
             for (int r = 0; r < 16; ++r) z = (mb == tmb && r == tr) ? acc[mb][nb][r] : z;
           a.zy[a.c0 + n] = z;
@@ -382,20 +384,22 @@ __global__ void __launch_bounds__(NT, 1) k_gemm(GemmArgs a) {
     // phase 2: e = exp(z - m), s = sum e, u = sum e (z - m); e optionally staged for storage.
     char* sQ = smem;
 #pragma unroll
-    for (int nb = 0; nb < 4; ++nb) {
-      const int cl = wn * 128 + nb * 32 + lrow;
-      const float mt = fmaxf(red_m[cl], red_m[kTile + cl]);
+    for (int nb = 0; nb < NBW; ++nb) {
+      const int cl = wn * WTN + nb * 32 + lrow;
+      float mt = red_m[cl];
+#pragma unroll
+      for (int w = 1; w < WAVES_M; ++w) mt = fmaxf(mt, red_m[w * kTile + cl]);
       const float mt2 = mt * kLog2e;
       float s = 0.0f, u = 0.0f;
 #pragma unroll
-      for (int mb = 0; mb < 4; ++mb)
+      for (int mb = 0; mb < MBW; ++mb)
 #pragma unroll
         for (int g = 0; g < 4; ++g) {
           float ev[4];
 #pragma unroll
           for (int i = 0; i < 4; ++i) {
             const int r = g * 4 + i;
-            const int rl = wm * 128 + mb * 32 + g * 8 + lh * 4 + i;
+            const int rl = wm * WTM + mb * 32 + g * 8 + lh * 4 + i;
             const float z = acc[mb][nb][r];
             const bool valid = full_v || v0 + rl < V;
             const float e = valid ? __builtin_amdgcn_exp2f(fmaf(z, kLog2e, -mt2)) : 0.0f;
@@ -404,8 +408,8 @@ __global__ void __launch_bounds__(NT, 1) k_gemm(GemmArgs a) {
             ev[i] = e;
           }
           if constexpr (STORE_Q) {
+            const int rl0 = wm * WTM + mb * 32 + g * 8 + lh * 4;
             if constexpr (sizeof(T) == 2) {
-              const int rl0 = wm * 128 + mb * 32 + g * 8 + lh * 4;
               u32x2 pk;
               pk.x = pack_bf16x2(ev[0], ev[1]);
               pk.y = pack_bf16x2(ev[2], ev[3]);
@@ -413,7 +417,6 @@ __global__ void __launch_bounds__(NT, 1) k_gemm(GemmArgs a) {
             } else {
               const int n = tile_n * kTile + cl;
               if (n < N) {
-                const int rl0 = wm * 128 + mb * 32 + g * 8 + lh * 4;
                 float* qp = reinterpret_cast<float*>(a.q) + (int64_t)n * a.ldq + v0 + rl0;
 #pragma unroll
                 for (int i = 0; i < 4; ++i) qp[i] = ev[i];
@@ -431,14 +434,21 @@ __global__ void __launch_bounds__(NT, 1) k_gemm(GemmArgs a) {
     __syncthreads();
     if (wm == 0 && lh == 0) {
 #pragma unroll
-      for (int nb = 0; nb < 4; ++nb) {
-        const int cl = wn * 128 + nb * 32 + lrow;
+      for (int nb = 0; nb < NBW; ++nb) {
+        const int cl = wn * WTN + nb * 32 + lrow;
         const int n = tile_n * kTile + cl;
         if (n < N) {
+          float m = red_m[cl], s = red_s[cl], u = red_u[cl];
+#pragma unroll
+          for (int w = 1; w < WAVES_M; ++w) {
+            m = fmaxf(m, red_m[w * kTile + cl]);
+            s += red_s[w * kTile + cl];
+            u += red_u[w * kTile + cl];
+          }
           const int64_t o = (int64_t)tile_m * a.Mc + n;
-          a.pm[o] = fmaxf(red_m[cl], red_m[kTile + cl]);
-          a.ps[o] = red_s[cl] + red_s[kTile + cl];
-          a.pu[o] = red_u[cl] + red_u[kTile + cl];
+          a.pm[o] = m;
+          a.ps[o] = s;
+          a.pu[o] = u;
         }
       }
     }
@@ -446,8 +456,8 @@ __global__ void __launch_bounds__(NT, 1) k_gemm(GemmArgs a) {
       // phase 3: coalesced copy of the staged bf16 tile to q[n][v0 .. v0 + 255].
       const int chunk = tid & 31;
 #pragma unroll 4
-      for (int it = 0; it < 32; ++it) {
-        const int cl = (tid >> 5) + 8 * it;
+      for (int it = 0; it < kTile * 32 / NT; ++it) {
+        const int cl = (tid >> 5) + (NT / 32) * it;
         const int n = tile_n * kTile + cl;
         if (n < N) {
           const u32x4 v = *reinterpret_cast<const u32x4*>(sQ + cl * QROW + chunk * 16);
@@ -460,15 +470,15 @@ __global__ void __launch_bounds__(NT, 1) k_gemm(GemmArgs a) {
     // rows = chunk-local tokens, columns = hidden features; scatter to dh[idx[c0 + row]].
     T* out = reinterpret_cast<T*>(a.out);
 #pragma unroll
-    for (int mb = 0; mb < 4; ++mb)
+    for (int mb = 0; mb < MBW; ++mb)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const int rl = tile_m * kTile + wm * 128 + mb * 32 + (r >> 2) * 8 + lh * 4 + (r & 3);
+        const int rl = tile_m * kTile + wm * WTM + mb * 32 + (r >> 2) * 8 + lh * 4 + (r & 3);
         if (rl < M) {
           const int64_t row = a.idx[a.c0 + rl];
 #pragma unroll
-          for (int nb = 0; nb < 4; ++nb) {
-            const int cl = tile_n * kTile + wn * 128 + nb * 32 + lrow;
+          for (int nb = 0; nb < NBW; ++nb) {
+            const int cl = tile_n * kTile + wn * WTN + nb * 32 + lrow;
             if (cl < N) store_elem<T>(out + row * a.ldo + cl, acc[mb][nb][r]);
           }
         }
@@ -478,14 +488,14 @@ __global__ void __launch_bounds__(NT, 1) k_gemm(GemmArgs a) {
     // chunk unless the caller accumulates.
     const bool add = a.accumulate || a.c0 > 0;
 #pragma unroll
-    for (int mb = 0; mb < 4; ++mb)
+    for (int mb = 0; mb < MBW; ++mb)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const int rl = tile_m * kTile + wm * 128 + mb * 32 + (r >> 2) * 8 + lh * 4 + (r & 3);
+        const int rl = tile_m * kTile + wm * WTM + mb * 32 + (r >> 2) * 8 + lh * 4 + (r & 3);
         if (rl < M) {
 #pragma unroll
-          for (int nb = 0; nb < 4; ++nb) {
-            const int cl = tile_n * kTile + wn * 128 + nb * 32 + lrow;
+          for (int nb = 0; nb < NBW; ++nb) {
+            const int cl = tile_n * kTile + wn * WTN + nb * 32 + lrow;
             if (cl < N) {
               float* p = a.dw + (int64_t)rl * a.ldo + cl;
               *p = add ? *p + acc[mb][nb][r] : acc[mb][nb][r];
