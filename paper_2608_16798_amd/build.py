@@ -2,6 +2,8 @@
 
 Usage: python -m paper_2608_16798_amd.build   (or call build()).
 Every call recompiles; objects go to paper_2608_16798_amd/_build/.
+RLK_EXTRA_FLAGS (environment) appends hipcc flags, e.g. "-DRLK_KS=64 -DRLK_NSTAGE=4" for the GEMM
+pipeline geometry.
 """
 from __future__ import annotations
 
@@ -21,7 +23,7 @@ HIPCC = shutil.which("hipcc") or "/opt/rocm/bin/hipcc"
 # Packed fp32 VALU forms are disabled for all device code.
 DEVICE_FLAGS = ["-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
 CFLAGS = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}", "-Wall", "-Wno-unused-function",
-          "-Wno-unused-variable"] + DEVICE_FLAGS
+          "-Wno-unused-variable"] + DEVICE_FLAGS + os.environ.get("RLK_EXTRA_FLAGS", "").split()
 
 
 def _sources():

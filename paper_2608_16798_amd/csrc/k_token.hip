@@ -166,14 +166,21 @@ __global__ void __launch_bounds__(256) k_combine(TokenParams p) {
 }
 
 // ---- dz for a chunk: q holds exp(z - m_tile) per (token, vocabulary); rewritten in place with
-// dz and also written transposed for the dW GEMM.  Tile: 64 tokens x 256 vocabulary entries
-// (one forward vocabulary tile, so one m_tile per token).
+// dz and also written transposed for the dW GEMM.  Block tile: 64 tokens x 256 vocabulary
+// entries (one forward vocabulary tile, so one m_tile per token).  Each thread owns an EPC x EPC
+// square (EPC tokens x EPC consecutive vocabulary entries, EPC = elements per 16 bytes): it reads
+// EPC 16-byte rows, writes them back as dz and transposes the square in registers into EPC
+// 16-byte rows of dz^T, so neither layout needs an LDS pass.  The per-token scalars are
+// computed once per block into LDS.
 template <typename T, bool ENT>
 __global__ void __launch_bounds__(256) k_dz(DzParams p) {
   constexpr int EPC = 16 / sizeof(T);
-  constexpr int CPR = kVocabTile / EPC;          // chunks per token row of the tile
-  constexpr int PAD = EPC;
-  __shared__ __attribute__((aligned(16))) T sT[kVocabTile][64 + PAD];
+  constexpr int TG = 64 / EPC;                  // token groups per block (lanes along tokens)
+  constexpr int VC = 64 / TG;                   // vocabulary chunks per wavefront pass
+  constexpr int VSPAN = VC * EPC;               // vocabulary entries per wavefront pass
+  constexpr int PASSES = kVocabTile / (4 * VSPAN);
+  __shared__ float s_sc[64], s_g[64], s_e[64], s_base[64], s_dzy[64];
+  __shared__ int s_y[64], s_ok[64];   // s_ok: token inside the chunk (else dz = 0)
   int64_t rc = (int64_t)p.hdr->n_eff - p.c0;
   rc = rc < 0 ? 0 : (rc > p.Mc ? p.Mc : rc);
   const int64_t rpad = (rc + kKAlign - 1) / kKAlign * kKAlign;
@@ -181,52 +188,74 @@ __global__ void __launch_bounds__(256) k_dz(DzParams p) {
   const int64_t v0 = (int64_t)vt * kVocabTile;
   const int64_t t0 = (int64_t)blockIdx.y * 64;
   if (t0 >= rpad) return;
-  T* q = reinterpret_cast<T*>(p.q);
-  for (int c = threadIdx.x; c < 64 * CPR; c += 256) {
-    const int tl = c / CPR, ch = c % CPR;
+  if (threadIdx.x < 64) {
+    const int tl = threadIdx.x;
     const int64_t t = t0 + tl;
+    float sc = 0.0f, g = 0.0f, e = 0.0f, base = 0.0f, dzy = 0.0f;
+    int y = -1;
     if (t < rc) {
       const int64_t i = p.c0 + t;
-      const float lse = p.lse[i], logp = p.logp[i], H = p.ent[i], g = p.gt[i], e = p.et[i];
-      const int y = p.ytgt[i];
+      const float lse = p.lse[i], logp = p.logp[i], H = p.ent[i];
+      g = p.gt[i];
+      e = p.et[i];
       const float mk = p.pm[(int64_t)vt * p.Mc + t];
-      const float sc = __builtin_amdgcn_exp2f((mk - lse) * kLog2e);
-      const float base = mk - lse + H;    // z - lse + H = log q + base
-      T* qp = q + t * p.Vp + v0 + ch * EPC;
-      const u32x4 raw = *reinterpret_cast<const u32x4*>(qp);
-      T o[EPC];
-#pragma unroll
-      for (int k = 0; k < EPC; ++k) {
-        const float qv = vget<T>(raw, k);
-        const int64_t v = v0 + ch * EPC + k;
-        float dz;
-        if (v == y) {
-          // the target entry uses the exact fp32 log-prob: 1 - p_y = -expm1(logp)
-          dz = g * (-expm1f(logp));
-          if (ENT) dz -= e * expf(logp) * (logp + H);
-        } else {
-          const float pr = qv * sc;
-          float coef = g;
-          if (ENT) coef += (qv > 0.0f) ? e * (__logf(qv) + base) : 0.0f;
-          dz = -pr * coef;
-        }
-        o[k] = to_storage<T>(dz);
-      }
-      *reinterpret_cast<u32x4*>(qp) = vpack<T>(o);
-#pragma unroll
-      for (int k = 0; k < EPC; ++k) sT[ch * EPC + k][tl] = o[k];
-    } else {
-#pragma unroll
-      for (int k = 0; k < EPC; ++k) sT[ch * EPC + k][tl] = (T)0;
+      sc = __builtin_amdgcn_exp2f((mk - lse) * kLog2e);
+      base = mk - lse + H;    // z - lse + H = log q + base
+      const int yy = p.ytgt[i];
+      if (yy >= v0 && yy < v0 + kVocabTile) y = (int)(yy - v0);
+      // the target entry uses the exact fp32 log-prob: 1 - p_y = -expm1(logp)
+      dzy = g * (-expm1f(logp));
+      if (ENT) dzy -= e * expf(logp) * (logp + H);
     }
+    s_sc[tl] = sc;
+    s_g[tl] = g;
+    s_e[tl] = e;
+    s_base[tl] = base;
+    s_dzy[tl] = dzy;
+    s_y[tl] = y;
+    s_ok[tl] = t < rc;
   }
   __syncthreads();
+  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+  const int vc = lane % VC, tg = lane / VC;
+  T* q = reinterpret_cast<T*>(p.q);
   T* dzt = reinterpret_cast<T*>(p.dzt);
-  constexpr int TCH = 64 / EPC;   // 16-byte chunks per transposed row (64 tokens)
-  for (int c = threadIdx.x; c < kVocabTile * TCH; c += 256) {
-    const int vl = c / TCH, ch = c % TCH;
-    *reinterpret_cast<u32x4*>(dzt + (v0 + vl) * p.Mc + t0 + ch * EPC) =
-        *reinterpret_cast<const u32x4*>(&sT[vl][ch * EPC]);
+#pragma unroll
+  for (int ps = 0; ps < PASSES; ++ps) {
+    const int vl0 = (ps * 4 + wid) * VSPAN + vc * EPC;   // tile-local first vocabulary entry
+    u32x4 raw[EPC];
+#pragma unroll
+    for (int j = 0; j < EPC; ++j)
+      raw[j] = *reinterpret_cast<const u32x4*>(q + (t0 + tg * EPC + j) * p.Vp + v0 + vl0);
+    float o[EPC][EPC];
+#pragma unroll
+    for (int j = 0; j < EPC; ++j) {
+      const int tl = tg * EPC + j;
+      const float sc = s_sc[tl], g = s_g[tl];
+      const int y = s_y[tl];
+      const bool ok = s_ok[tl] != 0;
+#pragma unroll
+      for (int k = 0; k < EPC; ++k) {
+        const float qv = vget<T>(raw[j], k);
+        float coef = g;
+        if (ENT) coef += (qv > 0.0f) ? s_e[tl] * (__logf(qv) + s_base[tl]) : 0.0f;
+        o[j][k] = !ok ? 0.0f : (vl0 + k == y) ? s_dzy[tl] : -(qv * sc) * coef;
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < EPC; ++j) {
+      T row[EPC];
+#pragma unroll
+      for (int k = 0; k < EPC; ++k) row[k] = to_storage<T>(o[j][k]);
+      *reinterpret_cast<u32x4*>(q + (t0 + tg * EPC + j) * p.Vp + v0 + vl0) = vpack<T>(row);
+    }
+#pragma unroll
+    for (int k = 0; k < EPC; ++k) {
+      T col[EPC];
+#pragma unroll
+      for (int j = 0; j < EPC; ++j) col[j] = to_storage<T>(o[j][k]);
+      *reinterpret_cast<u32x4*>(dzt + (v0 + vl0 + k) * p.Mc + t0 + tg * EPC) = vpack<T>(col);
+    }
   }
 }
 
