@@ -77,11 +77,15 @@ __device__ __forceinline__ void sched_step() {
   }
 }
 
-// 16-byte-chunk XOR swizzle of an LDS row (CPR chunks): fragment reads of 8 or 16 consecutive
-// rows at one logical chunk touch distinct banks (for 32 and for 64 four-byte banks).
+// 16-byte-chunk XOR swizzle of an LDS row (CPR chunks).  A 16-byte fragment read serves 16 lanes
+// = 16 consecutive rows per cycle; with 128-byte rows two rows share one 256-byte bank window, and
+// (row parity, chunk ^ swz(row)) is distinct over the 16 rows, so the reads are conflict free.
+// swz depends on r mod 16 only: the fragment addresses of a wavefront's 32-row MFMA blocks then
+// differ by immediate offsets, and a copy's lane offset depends on its instruction only through
+// the instruction's parity.
 __device__ __forceinline__ int swz(int r) {
-  if constexpr (CPR == 8) return (r ^ (r >> 3)) & 7;
-  else return ((r >> 1) ^ (r >> 3)) & 3;
+  if constexpr (CPR == 8) return (r >> 1) & 7;
+  else return (r >> 1) & 3;
 }
 
 // s_waitcnt with only the vector-memory counter constrained (gfx9 encoding: vmcnt[3:0] in
@@ -199,7 +203,7 @@ __global__ void __launch_bounds__(NT) k_gemm(GemmArgs a) {
   if (!map_tile(tm, tn, tile_m, tile_n)) return;
 
   const int tid = threadIdx.x;
-  const int lane = tid & 63, wid = tid >> 6, wm = wid / WAVES_N, wn = wid % WAVES_N;
+  const int lane = tid & 63, wid = __builtin_amdgcn_readfirstlane(tid >> 6), wm = wid / WAVES_N, wn = wid % WAVES_N;
   const int lrow = lane & 31, lh = lane >> 5;
 
   // ---- operand panels as buffer resources: rows beyond M/N (and, with KTAIL, K chunks beyond K)
@@ -220,33 +224,40 @@ __global__ void __launch_bounds__(NT) k_gemm(GemmArgs a) {
   // [w * IPW * RPI, (w + 1) * IPW * RPI) of each operand with IPW instructions; lane l of
   // instruction j carries row (w * IPW + j) * RPI + l / CPR into LDS slot l % CPR, which holds the
   // logical 16-byte K chunk (l % CPR) ^ swz(row).
-  uint32_t voa[IPW], vob[IPW];
+  // The lane part of a copy's offset depends on the instruction only through its parity; the row
+  // part is uniform and goes into the scalar offset.
+  static_assert(RPI % 2 == 0 || RPI == 1, "copy geometry");
+  uint32_t voa[2], vob[2];
 #pragma unroll
-  for (int j = 0; j < IPW; ++j) {
+  for (int j = 0; j < 2; ++j) {
     const int row = (wid * IPW + j) * RPI + lane / CPR;
     const int chunk = (lane % CPR) ^ swz(row);
-    voa[j] = (uint32_t)row * lda_b + chunk * 16;
-    vob[j] = (uint32_t)row * ldb_b + chunk * 16;
+    voa[j] = (uint32_t)(lane / CPR) * lda_b + chunk * 16;
+    vob[j] = (uint32_t)(lane / CPR) * ldb_b + chunk * 16;
   }
-  auto dma = [&](int kt) {
+  // copies of slice kt for the rows owned by wavefront w
+  auto dma_w = [&](int kt, int w) {
     char* st = smem + (kt % NSTAGE) * STAGE_B;
     const uint32_t kb = (uint32_t)kt * KS;
 #pragma unroll
     for (int j = 0; j < IPW; ++j) {
-      uint32_t oa = voa[j], ob = vob[j];
+      const uint32_t r0 = (uint32_t)((w * IPW + j) * RPI);
+      uint32_t oa = voa[j & 1], ob = vob[j & 1];
       if constexpr (KTAIL) {
         // chunks past the end of K would read the next row: push them out of range (zero fill)
-        const int row = (wid * IPW + j) * RPI + lane / CPR;
+        const int row = (w * IPW + j) * RPI + lane / CPR;
         const uint32_t ck = kb + (((lane % CPR) ^ swz(row)) * 16);
         if ((int64_t)ck >= Kb) {
           oa = 0x80000000u;
           ob = 0x80000000u;
         }
       }
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(rsa, LDSP(st + (wid * IPW + j) * 1024), 16, oa, kb, 0, 0);
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(rsb, LDSP(st + OPND_B + (wid * IPW + j) * 1024), 16, ob, kb, 0, 0);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rsa, LDSP(st + (w * IPW + j) * 1024), 16, oa, kb + r0 * lda_b, 0, 0);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rsb, LDSP(st + OPND_B + (w * IPW + j) * 1024), 16, ob,
+                                               kb + r0 * ldb_b, 0, 0);
     }
   };
+  auto dma = [&](int kt) { dma_w(kt, wid); };
   // Fragment reads: lane (lrow, lh) takes logical K chunk 2 kk + lh of row r.
   auto frags = [&](int kt, int kk, u32x4 (&fa)[MBW], u32x4 (&fb)[NBW]) {
     const char* sA = smem + (kt % NSTAGE) * STAGE_B;
