@@ -5,6 +5,13 @@ in HBM: rlk_group_advantage + rlk_pg_loss_fwd_bwd (compaction, advantages, LM-he
 online log-softmax, loss, dz, dhidden and dW GEMMs).  Prints one JSON line.
 
   python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload qwen8b_bf16]
+
+HBM traffic of the GEMMs (the roofline's "traffic"): run one step twice under rocprofv3 counter
+collection, once with FETCH_SIZE and once with WRITE_SIZE, each with --calibrate-copy-mib so the
+same run holds a plain device copy of known size, then
+  python bench.py --traffic-summary FETCH.csv WRITE.csv [--workload ...]
+writes profiles/<kernel>_<workload>_traffic.txt (HBM bytes per launch, scaled by the copy's
+known/measured ratio, tagged with a digest of the kernel sources).
 """
 from __future__ import annotations
 
@@ -114,6 +121,84 @@ def cpu_baseline(cfg, inp, target_tokens: int):
             "seconds": dt}
 
 
+COPY_TAG = "neg"   # the calibration copy is torch.neg on fp32 (reads and writes its size once)
+KERNEL_KIND = {"0": "fwd_lse_gemm", "1": "dh_gemm", "2": "dw_gemm"}
+
+
+def _counter_rows(path):
+    import csv
+    import re
+
+    per = {}
+    for r in csv.DictReader(open(path)):
+        name = r["Kernel_Name"]
+        m = re.search(r"k_gemm<[^,]+, (\d)", name)
+        kind = KERNEL_KIND.get(m.group(1)) if m else ("copy" if COPY_TAG in name else None)
+        if kind is None:
+            continue
+        d = per.setdefault(kind, {})
+        d[r["Dispatch_Id"]] = d.get(r["Dispatch_Id"], 0.0) + float(r["Counter_Value"])
+    return per
+
+
+def traffic_summary(fetch_csv, write_csv, workload, copy_mib, cmd_fetch, cmd_write):
+    """Per-launch HBM bytes of the three GEMMs from FETCH_SIZE / WRITE_SIZE (KiB per dispatch),
+    each scaled by known / measured for the calibration copy in the same run."""
+    fetch, write = _counter_rows(fetch_csv), _counter_rows(write_csv)
+    known_kib = copy_mib * 1024.0
+    f_copy = max(fetch["copy"].values())
+    w_copy = max(write["copy"].values())
+    kf, kw = known_kib / f_copy, known_kib / w_copy
+    digest = kernel_source_digest()
+    paths = []
+    for kind in KERNEL_KIND.values():
+        if kind not in fetch or kind not in write:
+            continue
+        n = len(fetch[kind])
+        fk = sum(fetch[kind].values()) / n
+        wk = sum(write[kind].values()) / len(write[kind])
+        hbm = (fk * kf + wk * kw) * 1024.0
+        path = os.path.join(PROFILES, f"{kind}_{workload}_traffic.txt")
+        with open(path, "w") as f:
+            f.write(f"# HBM traffic of {kind} on the {workload} workload, one step, rocprofv3 counters\n")
+            f.write(f"# fetch pass: {cmd_fetch}\n# write pass: {cmd_write}\n")
+            f.write(f"# summary: python bench.py --traffic-summary <fetch csv> <write csv> --workload {workload} "
+                    f"--calibrate-copy-mib {copy_mib}\n")
+            f.write(f"launches_per_step: {n}\n")
+            f.write(f"fetch_kib_per_launch_raw: {fk:.1f}\nwrite_kib_per_launch_raw: {wk:.1f}\n")
+            f.write(f"copy_known_kib: {known_kib:.0f}\ncopy_fetch_kib: {f_copy:.1f}\ncopy_write_kib: {w_copy:.1f}\n")
+            f.write(f"fetch_scale: {kf:.4f}\nwrite_scale: {kw:.4f}\n")
+            f.write(f"hbm_bytes_per_launch: {hbm:.0f}\n")
+            f.write(f"kernel_source_digest: {digest}\n")
+        paths.append(path)
+    return paths
+
+
+def stats_summary(stats_csv, title, cmd):
+    """Text table of the rlk kernels from a rocprofv3 --stats kernel summary CSV."""
+    import csv
+    import re
+
+    def short(n):
+        m = re.search(r"k_gemm<rlk::(\w+), (\d), (\w+), (\w+)>", n)
+        if m:
+            kind = ["fwd_lse", "dh", "dw"][int(m.group(2))]
+            return f"k_gemm<{m.group(1)},{kind},store_q={m.group(3)},ktail={m.group(4)}>"
+        m = re.search(r"rlk::\(anonymous namespace\)::(k_\w+)(<[^>(]*>)?", n)
+        return (m.group(1) + (m.group(2) or "")) if m else None
+
+    out = [f"# {title}", f"# command: {cmd}",
+           "# summary: python bench.py --stats-summary <kernel_stats.csv> (rlk kernels only; microseconds)",
+           f"{'kernel':58s} {'calls':>6s} {'total_us':>12s} {'avg_us':>10s} {'min_us':>10s} {'max_us':>10s} {'pct':>6s}"]
+    for r in csv.DictReader(open(stats_csv)):
+        k = short(r["Name"])
+        if k:
+            out.append(f"{k:58s} {int(r['Calls']):6d} {float(r['TotalDurationNs']) / 1e3:12.1f} "
+                       f"{float(r['AverageNs']) / 1e3:10.1f} {float(r['MinNs']) / 1e3:10.1f} "
+                       f"{float(r['MaxNs']) / 1e3:10.1f} {float(r['Percentage']):6.2f}")
+    return "\n".join(out) + "\n"
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -125,7 +210,25 @@ def main():
     ap.add_argument("--cpu-tokens", type=int, default=1024)
     ap.add_argument("--no-kernel-events", action="store_true",
                     help="time the steps without per-kernel HIP events (roofline then null)")
+    ap.add_argument("--calibrate-copy-mib", type=int, default=0,
+                    help="run a plain device copy of this many MiB first (counter calibration)")
+    ap.add_argument("--traffic-summary", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
+                    help="write profiles/<kernel>_<workload>_traffic.txt from two counter runs and exit")
+    ap.add_argument("--pmc-commands", nargs=2, default=("", ""), help=argparse.SUPPRESS)
+    ap.add_argument("--stats-summary", nargs=3, metavar=("STATS_CSV", "TITLE", "COMMAND"),
+                    help="print a text table of the rlk kernels from a rocprofv3 --stats CSV and exit")
     args = ap.parse_args()
+
+    if args.stats_summary:
+        sys.stdout.write(stats_summary(*args.stats_summary))
+        return
+
+    if args.traffic_summary:
+        if args.calibrate_copy_mib <= 0:
+            raise SystemExit("--traffic-summary needs the --calibrate-copy-mib size the runs used")
+        for p in traffic_summary(*args.traffic_summary, args.workload, args.calibrate_copy_mib, *args.pmc_commands):
+            print(p)
+        return
 
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only: this build has no multi-GPU path (--gpus {args.gpus} requested)",
@@ -170,6 +273,14 @@ def main():
         rlk.pg_loss_fwd_bwd(inp["h"], inp["W"], inp["targets"], inp["mask"], inp["cu"], inp["old"], inp["rewards"],
                             inp["gid"], params, loss=loss, dhidden=dh, dW=dW, stats=stats, ws=ws, stream=stream)
 
+    if args.calibrate_copy_mib > 0:
+        n = args.calibrate_copy_mib * (1 << 20) // 4
+        src = torch.ones(n, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        torch.neg(src, out=dst)   # reads and writes calibrate_copy_mib MiB once
+        torch.cuda.synchronize()
+        del src, dst
     log(f"[bench] warmup {args.warmup} step(s), N={N} R={R} ws={ws.numel() / 2**30:.1f} GiB")
     for _ in range(args.warmup):
         step()
