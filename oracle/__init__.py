@@ -13,6 +13,8 @@ from .rl_oracle import (  # noqa: F401
     token_logprob,
     token_weights,
     surrogate,
+    tis_weight,
+    kl_sampled,
     pg_loss_fwd_bwd,
     sampled_rows,
 )

@@ -34,7 +34,14 @@ Readings where the paper is silent (each one is stated where it is applied):
     bound the gradient passes (clipped only on strict inequality);
   * optional entropy bonus: objective += c_ent * H_t under the same mask and
     aggregation, H_t the full-vocabulary Shannon entropy in nats;
-  * the KL term and truncated importance sampling are off (beta = 0, w_t = 1);
+  * the KL term of the GRPO objective (Sec. 2.3.2) is optional (beta = 0 by
+    default); when on, D_KL(pi_theta || pi_ref) at a sampled token is the
+    estimator r/p - log(r/p) - 1 of the GRPO work the paper builds on, from the
+    reference policy's log-prob of the sampled token (no second LM head);
+  * token-level truncated importance sampling (Sec. 3.2.4) is optional (off by
+    default); when on, w_t = min(exp(old_t - rollout_t), c_bar) scales the whole
+    loss of token t (surrogate, entropy and KL terms) and is held constant in
+    the gradient;
   * a rollout with no policy tokens contributes 0 to its group's sum but still
     counts in G_q and in mu/sigma;
   * group_id < 0 marks an excluded rollout: removed from mu, sigma, G_q, Q and
@@ -169,6 +176,19 @@ def surrogate(logp, old_logp, adv_tok, eps_low, eps_high):
     return s, rho, clipped
 
 
+def tis_weight(old_logp, rollout_logp, cap):
+    """Sec. 3.2.4, token-level truncated importance-sampling weight:
+    w_t = min(exp(log pi_old - log pi_rollout), c_bar)."""
+    return np.minimum(np.exp(_f64(old_logp) - _f64(rollout_logp)), float(cap))
+
+
+def kl_sampled(logp, ref_logp):
+    """KL(pi_theta || pi_ref) at a sampled token, the estimator pi_ref/pi - log(pi_ref/pi) - 1
+    (GRPO objective, Sec. 2.3.2).  Returns the estimate and its derivative w.r.t. log pi_theta."""
+    r = _f64(ref_logp) - _f64(logp)
+    return np.expm1(r) - r, -np.expm1(r)
+
+
 def token_weights(tok_rollout, n_pol, gi, G, n_groups, agg=AGG_SEQ, norm_override=None):
     """d loss / d (s_t + c H_t) per compacted token (negative: loss = -objective).
 
@@ -211,11 +231,14 @@ def _aggregate(val, tok_rollout, n_pol, gi, G, n_groups, R, agg, norm_override):
 # --------------------------------------------------------------------------
 def pg_loss_fwd_bwd(h, W, targets, mask, cu_seqlens, old_logp, rewards, group_ids, *,
                     eps_low=0.2, eps_high=0.2, adv_eps=1e-6, entropy_coef=0.0, agg=AGG_SEQ,
-                    norm_override=None, grads=True, block: int = 128):
+                    norm_override=None, rollout_logp=None, tis_cap=None, ref_logp=None, kl_coef=0.0,
+                    grads=True, block: int = 128):
     """Loss, per-token outputs and gradients w.r.t. hidden states and the LM-head weight.
 
     h [N, d], W [V, d] (any float dtype, evaluated in fp64), targets [N], mask [N]
-    (None = all policy), cu_seqlens [R+1], old_logp [N], rewards [R], group_ids [R].
+    (None = all policy), cu_seqlens [R+1], old_logp [N], rewards [R], group_ids [R];
+    rollout_logp [N] with tis_cap switches on truncated importance sampling, ref_logp [N]
+    with kl_coef > 0 the KL term.
     """
     h = np.asarray(h)
     W64 = _f64(W)
@@ -230,6 +253,8 @@ def pg_loss_fwd_bwd(h, W, targets, mask, cu_seqlens, old_logp, rewards, group_id
     adv, gi, Q, G = ga["adv"], ga["group_index"], ga["n_groups"], ga["G"]
     n = idx.shape[0]
     omega = token_weights(tok_r, n_pol, gi, G, Q, agg, norm_override)
+    tis = tis_weight(old[idx], _f64(rollout_logp)[idx], tis_cap) if rollout_logp is not None else np.ones(n)
+    ref = _f64(ref_logp)[idx] if (ref_logp is not None and kl_coef) else None
 
     lse = np.zeros(n)
     logp = np.zeros(n)
@@ -237,6 +262,7 @@ def pg_loss_fwd_bwd(h, W, targets, mask, cu_seqlens, old_logp, rewards, group_id
     s = np.zeros(n)
     rho = np.zeros(n)
     clipped = np.zeros(n, dtype=bool)
+    kl = np.zeros(n)
     g = np.zeros(n)
     e = np.zeros(n)
     dh = np.zeros((N, d)) if grads else None
@@ -257,9 +283,14 @@ def pg_loss_fwd_bwd(h, W, targets, mask, cu_seqlens, old_logp, rewards, group_id
         H[b0:b1] = -(p * lp).sum(axis=1)
         sb, rb, cb = surrogate(logp[b0:b1], old[rows], adv[tok_r[b0:b1]], eps_low, eps_high)
         s[b0:b1], rho[b0:b1], clipped[b0:b1] = sb, rb, cb
-        # chain rule: dL/dlogp_t = omega_t A rho_t [not clipped]; dL/dH_t = omega_t c_ent
-        gb = omega[b0:b1] * adv[tok_r[b0:b1]] * rb * (~cb)
-        eb = omega[b0:b1] * entropy_coef
+        # chain rule (w = tis weight, constant): dL/dlogp_t = omega_t w_t (A rho_t [not clipped]
+        # - beta dKL_t/dlogp_t); dL/dH_t = omega_t w_t c_ent
+        dkl = np.zeros(b1 - b0)
+        if ref is not None:
+            kl[b0:b1], dkl = kl_sampled(logp[b0:b1], ref[b0:b1])
+        wb = omega[b0:b1] * tis[b0:b1]
+        gb = wb * (adv[tok_r[b0:b1]] * rb * (~cb) - kl_coef * dkl)
+        eb = wb * entropy_coef
         g[b0:b1], e[b0:b1] = gb, eb
         if grads:
             onehot = np.zeros_like(z)
@@ -269,14 +300,16 @@ def pg_loss_fwd_bwd(h, W, targets, mask, cu_seqlens, old_logp, rewards, group_id
             dh[rows] = dz @ W64
             dW += dz.T @ hb
 
-    val = s + entropy_coef * H
+    val = tis * (s + entropy_coef * H - kl_coef * kl)
     J = _aggregate(val, tok_r, n_pol, gi, G, Q, R, agg, norm_override)
-    Jpg = _aggregate(s, tok_r, n_pol, gi, G, Q, R, agg, norm_override)
+    Jpg = _aggregate(tis * s, tok_r, n_pol, gi, G, Q, R, agg, norm_override)
     stats = dict(
         loss=-J, pg_loss=-Jpg,
         entropy_mean=float(H.mean()) if n else 0.0,
         clip_frac=float(clipped.mean()) if n else 0.0,
         ratio_mean=float(rho.mean()) if n else 0.0,
+        kl_mean=float(kl.mean()) if n else 0.0,
+        tis_mean=float(tis.mean()) if n else 0.0,
         n_policy_tokens=int(n), n_groups=int(Q), n_valid_rollouts=int((gi >= 0).sum()))
     logp_full = np.zeros(N)
     H_full = np.zeros(N)
@@ -286,12 +319,12 @@ def pg_loss_fwd_bwd(h, W, targets, mask, cu_seqlens, old_logp, rewards, group_id
     lse_full[idx] = lse
     return dict(loss=-J, pg_loss=-Jpg, stats=stats, idx=idx, tok_rollout=tok_r, n_pol=n_pol,
                 adv=adv, group_index=gi, n_groups=Q, omega=omega, lse=lse, logp=logp, H=H,
-                rho=rho, clipped=clipped, g=g, e=e, logp_full=logp_full, entropy_full=H_full,
+                rho=rho, clipped=clipped, kl=kl, tis=tis, g=g, e=e, logp_full=logp_full, entropy_full=H_full,
                 lse_full=lse_full, dh=dh, dW=dW)
 
 
 def sampled_rows(h_rows, W, y_rows, old_rows, adv_rows, omega_rows, *, eps_low, eps_high,
-                 entropy_coef=0.0, block: int = 64):
+                 entropy_coef=0.0, tis_rows=None, ref_rows=None, kl_coef=0.0, block: int = 64):
     """Per-row forward and dhidden for selected policy rows of a large batch.
 
     A row's log-prob, entropy and dhidden depend only on that row and on
@@ -318,7 +351,10 @@ def sampled_rows(h_rows, W, y_rows, old_rows, adv_rows, omega_rows, *, eps_low, 
         A = _f64(adv_rows[b0:b1])
         _, rb, cb = surrogate(lpy, old_rows[b0:b1], A, eps_low, eps_high)
         om = _f64(omega_rows[b0:b1])
-        gb = om * A * rb * (~cb)
+        if tis_rows is not None:
+            om = om * _f64(tis_rows[b0:b1])
+        dkl = kl_sampled(lpy, ref_rows[b0:b1])[1] if (ref_rows is not None and kl_coef) else 0.0
+        gb = om * (A * rb * (~cb) - kl_coef * dkl)
         eb = om * entropy_coef
         onehot = np.zeros_like(z)
         onehot[ar, y[b0:b1]] = 1.0

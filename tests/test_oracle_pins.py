@@ -413,3 +413,91 @@ def test_gradient_invariants():
     out3 = _loss(b3, **kw)
     assert out3["loss"] == out["loss"]
     np.testing.assert_array_equal(out3["dW"], out["dW"])
+
+
+# ------------------------------------------- truncated IS (Sec. 3.2.4) and the KL term (Sec. 2.3.2)
+def _with_old_from_current(seed, sigma=0.25, **kw):
+    b = tiny_batch(seed, **kw)
+    lse, lp, H = O.token_logprob(b["h"], b["W"], b["targets"])
+    b["old_logp"] = lp + np.random.default_rng(seed + 1).standard_normal(lp.shape) * sigma
+    return b
+
+
+def test_tis_identity_when_rollout_equals_old():
+    b = _with_old_from_current(30, excluded=(1,))
+    kw = dict(eps_low=0.2, eps_high=0.28, entropy_coef=0.05)
+    plain = _loss(b, **kw)
+    tis = _loss(b, rollout_logp=b["old_logp"].copy(), tis_cap=2.0, **kw)
+    assert tis["loss"] == plain["loss"]
+    np.testing.assert_array_equal(tis["dh"], plain["dh"])
+    np.testing.assert_array_equal(tis["dW"], plain["dW"])
+    assert tis["stats"]["tis_mean"] == 1.0
+
+
+@pytest.mark.parametrize("shift,cap,expect", [(0.4, 5.0, math.exp(0.4)), (3.0, 2.5, 2.5), (-0.7, 4.0, math.exp(-0.7))])
+def test_tis_constant_weight_scales_the_whole_token_loss(shift, cap, expect):
+    # rollout = old - shift on every token: w_t = min(e^shift, cap) is one constant, so the loss
+    # (surrogate, entropy and KL terms alike) and both gradients scale by exactly that constant
+    b = _with_old_from_current(31, excluded=(3,))
+    ref = b["old_logp"] - 0.3
+    kw = dict(eps_low=0.2, eps_high=0.28, entropy_coef=0.07, ref_logp=ref, kl_coef=0.05)
+    plain = _loss(b, **kw)
+    tis = _loss(b, rollout_logp=b["old_logp"] - shift, tis_cap=cap, **kw)
+    np.testing.assert_allclose(tis["loss"], expect * plain["loss"], rtol=1e-12)
+    np.testing.assert_allclose(tis["pg_loss"], expect * plain["pg_loss"], rtol=1e-12)
+    np.testing.assert_allclose(tis["dh"], expect * plain["dh"], rtol=1e-10, atol=1e-15)
+    np.testing.assert_allclose(tis["dW"], expect * plain["dW"], rtol=1e-10, atol=1e-15)
+
+
+def test_kl_sampled_estimator_is_unbiased_by_enumeration():
+    # E_{a ~ p}[q_a/p_a - log(q_a/p_a) - 1] = KL(p || q) exactly, summing over the whole vocabulary
+    rng = np.random.default_rng(32)
+    for _ in range(5):
+        zp, zq = rng.standard_normal(24) * 2.0, rng.standard_normal(24) * 2.0
+        lp = zp - np.log(np.exp(zp).sum())
+        lq = zq - np.log(np.exp(zq).sum())
+        est, _ = O.kl_sampled(lp, lq)
+        assert np.all(est >= 0)
+        kl_exact = float((np.exp(lp) * (lp - lq)).sum())
+        np.testing.assert_allclose(float((np.exp(lp) * est).sum()), kl_exact, rtol=1e-12)
+    est, d = O.kl_sampled(np.array([-1.3]), np.array([-1.3]))
+    assert est[0] == 0.0 and d[0] == 0.0
+
+
+def test_kl_term_enters_the_loss_with_minus_beta():
+    # at rho = 1 with zero advantages (all rewards equal) the loss is beta times the mean sampled KL
+    b = _with_old_from_current(33, sigma=0.0)
+    b["rewards"][:] = 0.5
+    lse, lp, H = O.token_logprob(b["h"], b["W"], b["targets"])
+    ref = lp + np.random.default_rng(34).standard_normal(lp.shape) * 0.5
+    out = _loss(b, agg=O.AGG_TOKEN, ref_logp=ref, kl_coef=0.1)
+    idx = out["idx"]
+    r = ref[idx] - lp[idx]
+    np.testing.assert_allclose(out["loss"], 0.1 * np.mean(np.exp(r) - r - 1.0), rtol=1e-12)
+    np.testing.assert_allclose(out["stats"]["kl_mean"], np.mean(np.exp(r) - r - 1.0), rtol=1e-12)
+
+
+@pytest.mark.parametrize("agg", [O.AGG_SEQ, O.AGG_TOKEN])
+def test_tis_and_kl_gradients_match_finite_differences(agg):
+    b = _with_old_from_current(35, excluded=(4,), sigma=0.4)
+    b = _kink_safe(b, 0.2, 0.28)
+    rng = np.random.default_rng(36)
+    rollout = b["old_logp"] + rng.standard_normal(b["old_logp"].shape) * 0.6
+    ref = b["old_logp"] + rng.standard_normal(b["old_logp"].shape) * 0.5
+    kw = dict(eps_low=0.2, eps_high=0.28, agg=agg, entropy_coef=0.03, rollout_logp=rollout, tis_cap=1.5,
+              ref_logp=ref, kl_coef=0.2)
+    out = _loss(b, **kw)
+    assert 0 < out["stats"]["clip_frac"] < 1
+    assert np.any(out["tis"] == 1.5) and np.any(out["tis"] < 1.5)   # both sides of the cap
+    step = 1e-6
+    for name, grad in (("h", out["dh"]), ("W", out["dW"])):
+        X = b[name]
+        for ij in [tuple(rng.integers(0, s) for s in X.shape) for _ in range(20)]:
+            bp = dict(b)
+            bp[name] = X.copy()
+            bp[name][ij] += step
+            lp_ = _loss(bp, grads=False, **kw)["loss"]
+            bp[name][ij] -= 2 * step
+            lm_ = _loss(bp, grads=False, **kw)["loss"]
+            fd = (lp_ - lm_) / (2 * step)
+            assert abs(fd - grad[ij]) <= 1e-6 * max(1.0, abs(grad).max()), (name, ij, fd, grad[ij])

@@ -10,7 +10,8 @@ reproducible bit-for-bit on any host; the large float tensors (hidden states
 and LM-head weights) come from torch's generator on the requested device.
 """
 from .configs import CONFIGS, Config, get_config, scaled_config
-from .gen import Structure, make_structure, make_tensors, old_logp_from_anchor, sample_policy_rows
+from .gen import (Structure, make_structure, make_tensors, old_logp_from_anchor, perturbed_logps,
+                  sample_policy_rows)
 
 __all__ = [
     "CONFIGS",
@@ -21,5 +22,6 @@ __all__ = [
     "make_structure",
     "make_tensors",
     "old_logp_from_anchor",
+    "perturbed_logps",
     "sample_policy_rows",
 ]

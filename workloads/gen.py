@@ -146,6 +146,16 @@ def old_logp_from_anchor(anchor: np.ndarray, st: Structure) -> np.ndarray:
     return out.astype(np.float32)
 
 
+def perturbed_logps(old: np.ndarray, st: Structure, sigma: float, seed: int) -> np.ndarray:
+    """Log-probs of another policy for the same sampled tokens (the inference engine's
+    rollout log-probs, or a reference policy's): old + sigma * N(0,1) on policy rows, 0 on masked
+    rows (float32, seeded)."""
+    rng = np.random.Generator(np.random.PCG64(seed))
+    noise = rng.standard_normal(np.asarray(old).shape[0])
+    out = np.asarray(old, dtype=np.float64) + float(sigma) * noise
+    return np.where(st.mask.astype(bool), out, 0.0).astype(np.float32)
+
+
 def sample_policy_rows(candidates: np.ndarray, k: int, seed: int) -> np.ndarray:
     """k distinct rows drawn (seeded) from the given candidate positions, sorted."""
     rng = np.random.Generator(np.random.PCG64(seed))
