@@ -57,11 +57,10 @@ def build_inputs(cfg, device="cuda"):
 
 
 def kernel_source_digest() -> str:
-    d = os.path.join(ROOT, "paper_2608_16798_amd", "csrc")
+    """Digest of the source of the GEMM kernels (the roofline kernels): counter summaries taken
+    from other sources no longer describe them."""
     h = hashlib.sha256()
-    for f in sorted(os.listdir(d)):
-        if f.endswith((".hip", ".h")):
-            h.update(open(os.path.join(d, f), "rb").read())
+    h.update(open(os.path.join(ROOT, "paper_2608_16798_amd", "csrc", "k_gemm.hip"), "rb").read())
     return h.hexdigest()[:16]
 
 

@@ -47,7 +47,7 @@
 extern "C" {
 #endif
 
-#define RLK_VERSION 1
+#define RLK_VERSION 2
 
 typedef int32_t rlk_status_t;
 enum {
@@ -94,7 +94,19 @@ typedef struct {
   double norm_override; /* > 0: replaces Q (SEQ) or the policy-token count (TOKEN) so that
                            micro-batched calls add up to the one-call gradient */
   int64_t chunk_rows;   /* policy tokens per backward chunk, multiple of 256; 0 = auto */
-  int64_t reserved[4];  /* must be 0 */
+  /* Token-level truncated importance sampling (Sec. 3.2.4): with rollout_logp (device [N] f32,
+   * the inference engine's log-prob of each sampled token) the loss of token t is scaled by
+   * w_t = min(exp(old_logp[t] - rollout_logp[t]), tis_cap), held constant in the gradient.
+   * NULL = off (w_t = 1); tis_cap must then be 0, else finite and > 0. */
+  const float* rollout_logp;
+  /* KL term of the GRPO objective (Sec. 2.3.2): objective -= kl_coef * D_KL(pi_theta || pi_ref)
+   * per token, estimated at the sampled token as r - log r - 1 with r = pi_ref / pi_theta from
+   * ref_logp (device [N] f32, the reference policy's log-prob of each sampled token).
+   * kl_coef = 0: off (ref_logp unused); kl_coef > 0 needs ref_logp. */
+  const float* ref_logp;
+  float tis_cap;
+  float kl_coef;
+  int64_t reserved;     /* must be 0 */
 } rlk_pg_params_t;
 
 typedef struct {
@@ -106,6 +118,8 @@ typedef struct {
   int32_t n_groups;       /* Q */
   int32_t n_valid_rollouts;
   int64_t n_policy_tokens;/* N_eff */
+  float kl_mean;          /* token mean of the sampled-token KL estimate (0 when off) */
+  float tis_mean;         /* token mean of the importance weight w_t (1 when off) */
 } rlk_pg_stats_t;
 
 /* Workspace bytes needed by rlk_logprob_fwd (p == NULL) or by rlk_pg_loss_fwd_bwd (p

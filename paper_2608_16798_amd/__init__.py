@@ -35,13 +35,15 @@ class PgParams(ctypes.Structure):
     _fields_ = [("eps_low", ctypes.c_float), ("eps_high", ctypes.c_float), ("adv_eps", ctypes.c_float),
                 ("entropy_coef", ctypes.c_float), ("agg", ctypes.c_int32), ("accumulate_dW", ctypes.c_int32),
                 ("norm_override", ctypes.c_double), ("chunk_rows", ctypes.c_int64),
-                ("reserved", ctypes.c_int64 * 4)]
+                ("rollout_logp", ctypes.c_void_p), ("ref_logp", ctypes.c_void_p), ("tis_cap", ctypes.c_float),
+                ("kl_coef", ctypes.c_float), ("reserved", ctypes.c_int64)]
 
 
 class PgStats(ctypes.Structure):
     _fields_ = [("loss", ctypes.c_float), ("pg_loss", ctypes.c_float), ("entropy_mean", ctypes.c_float),
                 ("clip_frac", ctypes.c_float), ("ratio_mean", ctypes.c_float), ("n_groups", ctypes.c_int32),
-                ("n_valid_rollouts", ctypes.c_int32), ("n_policy_tokens", ctypes.c_int64)]
+                ("n_valid_rollouts", ctypes.c_int32), ("n_policy_tokens", ctypes.c_int64),
+                ("kl_mean", ctypes.c_float), ("tis_mean", ctypes.c_float)]
 
 
 class RlkError(RuntimeError):
@@ -120,7 +122,9 @@ def make_batch(hidden, W, cu_seqlens) -> Batch:
 
 
 def make_params(eps_low=0.2, eps_high=None, adv_eps=1e-6, entropy_coef=0.0, agg=AGG_SEQ, accumulate_dW=False,
-                norm_override=0.0, chunk_rows=0) -> PgParams:
+                norm_override=0.0, chunk_rows=0, tis_cap=0.0, kl_coef=0.0) -> PgParams:
+    """Loss parameters; the rollout / reference log-prob arrays of truncated importance sampling
+    and of the KL term are passed to pg_loss_fwd_bwd."""
     p = PgParams()
     p.eps_low = eps_low
     p.eps_high = eps_low if eps_high is None else eps_high
@@ -130,6 +134,8 @@ def make_params(eps_low=0.2, eps_high=None, adv_eps=1e-6, entropy_coef=0.0, agg=
     p.accumulate_dW = 1 if accumulate_dW else 0
     p.norm_override = float(norm_override or 0.0)
     p.chunk_rows = int(chunk_rows)
+    p.tis_cap = float(tis_cap)
+    p.kl_coef = float(kl_coef)
     return p
 
 
@@ -213,11 +219,17 @@ def group_advantage(rewards, group_ids, adv_eps=1e-6, adv=None, group_index=None
 
 def pg_loss_fwd_bwd(hidden, W, targets, mask, cu_seqlens, old_logp, rewards, group_ids, params: PgParams,
                     loss=None, dhidden=None, dW=None, logp_out=None, entropy_out=None, stats=None, ws=None,
-                    stream=None):
-    """Loss, dL/dhidden and dL/dW of the masked clipped policy-gradient objective."""
+                    stream=None, rollout_logp=None, ref_logp=None):
+    """Loss, dL/dhidden and dL/dW of the masked clipped policy-gradient objective.
+    rollout_logp / ref_logp ([N] fp32 device tensors or None) feed truncated importance sampling
+    (params.tis_cap) and the KL term (params.kl_coef)."""
     import torch
 
     lib = load_library()
+    if rollout_logp is not None or ref_logp is not None:
+        params = PgParams.from_buffer_copy(bytes(params))
+        params.rollout_logp = _ptr(rollout_logp)
+        params.ref_logp = _ptr(ref_logp)
     b = make_batch(hidden, W, cu_seqlens)
     dev = hidden.device
     if loss is None:

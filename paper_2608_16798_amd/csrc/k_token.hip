@@ -9,6 +9,9 @@
 // Sec. 2.3.2 with the tree rule of Sec. 3.2.3) or -1/sum M for the token mean (Sec. 2.3.1).
 // Backward: dL/dlogp_t = g_t = w_t A rho_t [not clipped], dL/dH_t = e_t = w_t c, and
 //   dz_tj = g_t ([j = y_t] - p_tj) - e_t p_tj (z_tj - lse_t + H_t).
+// Optional terms: truncated importance sampling (Sec. 3.2.4) multiplies w_t by
+// min(exp(old_t - rollout_t), c_bar); the KL term of the GRPO objective (Sec. 2.3.2) adds
+// -beta (e^r - r - 1), r = ref_t - logp_t, to the token's objective, so g_t gains w_t beta (e^r - 1).
 #include "rlk_internal.h"
 
 namespace rlk {
@@ -150,7 +153,8 @@ __global__ void __launch_bounds__(256) k_combine(TokenParams p) {
   if (p.with_grad) {
     const int r = p.tokr[i];
     const float A = p.adv[r];
-    const float rho = expf(logp - p.old_logp[row]);
+    const float old = p.old_logp[row];
+    const float rho = expf(logp - old);
     double w;
     if (p.agg == RLK_AGG_SEQ_MEAN_TOKEN_MEAN) {
       const double Qn = p.norm_override > 0 ? p.norm_override : (double)p.hdr->n_groups;
@@ -159,8 +163,13 @@ __global__ void __launch_bounds__(256) k_combine(TokenParams p) {
       const double Mn = p.norm_override > 0 ? p.norm_override : (double)p.hdr->n_eff;
       w = -1.0 / Mn;
     }
+    // truncated importance weight (Sec. 3.2.4): a constant factor on the token's whole loss
+    if (p.rollout_logp) w *= (double)fminf(expf(old - p.rollout_logp[row]), p.tis_cap);
     const bool clipped = (A > 0.0f && rho > 1.0f + p.eps_high) || (A < 0.0f && rho < 1.0f - p.eps_low);
-    p.gt[i] = clipped ? 0.0f : (float)(w * (double)A * (double)rho);
+    double dlogp = clipped ? 0.0 : (double)A * (double)rho;
+    // KL term: d/dlogp of -beta (e^r - r - 1), r = ref - logp, is beta (e^r - 1)
+    if (p.ref_logp) dlogp += (double)p.kl_coef * (double)expm1f(p.ref_logp[row] - logp);
+    p.gt[i] = (float)(w * dlogp);
     p.et[i] = (float)(w * (double)p.ent_coef);
   }
 }
@@ -260,102 +269,107 @@ __global__ void __launch_bounds__(256) k_dz(DzParams p) {
 }
 
 // ---- deterministic loss reduction: per-rollout fp64 sums, then one block over rollouts.
+// Per-rollout sums: [0] w s, [1] w H, [2] w KL (the loss terms, w = importance weight or 1),
+// [3] H, [4] rho, [5] clipped, [6] KL, [7] w (statistics).
 __global__ void __launch_bounds__(256) k_loss_rollout(LossParams p) {
-  __shared__ double sh[4][4];
+  __shared__ double sh[4][kRollSums];
   const int r = blockIdx.x;
   const int n = p.rnpol[r];
   const int s0 = p.rstart[r];
   const float A = p.adv[r];
-  double ss = 0.0, sH = 0.0, sR = 0.0, sC = 0.0;
+  double acc[kRollSums];
+#pragma unroll
+  for (int f = 0; f < kRollSums; ++f) acc[f] = 0.0;
   if (p.gidx[r] >= 0) {
     for (int k = threadIdx.x; k < n; k += 256) {
       const int i = s0 + k;
+      const int64_t row = p.idx[i];
       const float logp = p.logp[i];
-      const float rho = expf(logp - p.old_logp[p.idx[i]]);
+      const float old = p.old_logp[row];
+      const float rho = expf(logp - old);
       const float lo = 1.0f - p.eps_low, hi = 1.0f + p.eps_high;
       const float cr = fminf(fmaxf(rho, lo), hi);
       const float s = fminf(rho * A, cr * A);
       const bool clipped = (A > 0.0f && rho > hi) || (A < 0.0f && rho < lo);
-      ss += (double)s;
-      sH += (double)p.ent[i];
-      sR += (double)rho;
-      sC += clipped ? 1.0 : 0.0;
+      const double w = p.rollout_logp ? (double)fminf(expf(old - p.rollout_logp[row]), p.tis_cap) : 1.0;
+      double kl = 0.0;
+      if (p.ref_logp) {
+        const float d = p.ref_logp[row] - logp;
+        kl = (double)expm1f(d) - (double)d;
+      }
+      const double H = (double)p.ent[i];
+      acc[0] += w * (double)s;
+      acc[1] += w * H;
+      acc[2] += w * kl;
+      acc[3] += H;
+      acc[4] += (double)rho;
+      acc[5] += clipped ? 1.0 : 0.0;
+      acc[6] += kl;
+      acc[7] += w;
     }
   }
-  ss = wave_sum(ss);
-  sH = wave_sum(sH);
-  sR = wave_sum(sR);
-  sC = wave_sum(sC);
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  if (lane == 0) {
-    sh[w][0] = ss;
-    sh[w][1] = sH;
-    sh[w][2] = sR;
-    sh[w][3] = sC;
-  }
+#pragma unroll
+  for (int f = 0; f < kRollSums; ++f) acc[f] = wave_sum(acc[f]);
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  if (lane == 0)
+#pragma unroll
+    for (int f = 0; f < kRollSums; ++f) sh[wv][f] = acc[f];
   __syncthreads();
-  if (threadIdx.x < 4) {
+  if (threadIdx.x < kRollSums) {
     double t = 0.0;
     for (int k = 0; k < 4; ++k) t += sh[k][threadIdx.x];
-    p.rsum[(int64_t)r * 4 + threadIdx.x] = t;
+    p.rsum[(int64_t)r * kRollSums + threadIdx.x] = t;
   }
 }
 
 __global__ void __launch_bounds__(1024) k_loss_final(LossParams p) {
-  __shared__ double sh[16][5];
-  double J = 0.0, Jpg = 0.0, tH = 0.0, tR = 0.0, tC = 0.0;
-  const double c = (double)p.ent_coef;
+  constexpr int NF = 7;   // J, J_pg, then the sums of H, rho, clipped, KL, w
+  __shared__ double sh[16][NF];
+  double a[NF] = {0, 0, 0, 0, 0, 0, 0};
+  const double c = (double)p.ent_coef, beta = (double)p.kl_coef;
   for (int r = threadIdx.x; r < p.R; r += 1024) {
     const int q = p.gidx[r];
     const int n = p.rnpol[r];
     if (q < 0 || n == 0) continue;
-    const double* rs = p.rsum + (int64_t)r * 4;
-    if (p.agg == RLK_AGG_SEQ_MEAN_TOKEN_MEAN) {
-      const double denom = (double)n * (double)p.gsize[q];
-      J += (rs[0] + c * rs[1]) / denom;
-      Jpg += rs[0] / denom;
-    } else {
-      J += rs[0] + c * rs[1];
-      Jpg += rs[0];
-    }
-    tH += rs[1];
-    tR += rs[2];
-    tC += rs[3];
+    const double* rs = p.rsum + (int64_t)r * kRollSums;
+    const double denom = p.agg == RLK_AGG_SEQ_MEAN_TOKEN_MEAN ? (double)n * (double)p.gsize[q] : 1.0;
+    a[0] += (rs[0] + c * rs[1] - beta * rs[2]) / denom;
+    a[1] += rs[0] / denom;
+    a[2] += rs[3];
+    a[3] += rs[4];
+    a[4] += rs[5];
+    a[5] += rs[6];
+    a[6] += rs[7];
   }
-  J = wave_sum(J);
-  Jpg = wave_sum(Jpg);
-  tH = wave_sum(tH);
-  tR = wave_sum(tR);
-  tC = wave_sum(tC);
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  if (lane == 0) {
-    sh[w][0] = J;
-    sh[w][1] = Jpg;
-    sh[w][2] = tH;
-    sh[w][3] = tR;
-    sh[w][4] = tC;
-  }
+#pragma unroll
+  for (int f = 0; f < NF; ++f) a[f] = wave_sum(a[f]);
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  if (lane == 0)
+#pragma unroll
+    for (int f = 0; f < NF; ++f) sh[wv][f] = a[f];
   __syncthreads();
   if (threadIdx.x == 0) {
-    double a[5] = {0, 0, 0, 0, 0};
+    double t[NF] = {0, 0, 0, 0, 0, 0, 0};
     for (int k = 0; k < 16; ++k)
-      for (int f = 0; f < 5; ++f) a[f] += sh[k][f];
+      for (int f = 0; f < NF; ++f) t[f] += sh[k][f];
     const int n_eff = p.hdr->n_eff;
     const int Q = p.hdr->n_groups;
     double norm;
     if (p.agg == RLK_AGG_SEQ_MEAN_TOKEN_MEAN) norm = p.norm_override > 0 ? p.norm_override : (double)Q;
     else norm = p.norm_override > 0 ? p.norm_override : (double)n_eff;
     const bool empty = n_eff == 0 || Q == 0;
-    const float loss = empty ? 0.0f : (float)(-a[0] / norm);
-    const float pg = empty ? 0.0f : (float)(-a[1] / norm);
+    const float loss = empty ? 0.0f : (float)(-t[0] / norm);
+    const float pg = empty ? 0.0f : (float)(-t[1] / norm);
     if (p.loss) p.loss[0] = loss;
     if (p.stats) {
       rlk_pg_stats_t st;
       st.loss = loss;
       st.pg_loss = pg;
-      st.entropy_mean = n_eff ? (float)(a[2] / n_eff) : 0.0f;
-      st.ratio_mean = n_eff ? (float)(a[3] / n_eff) : 0.0f;
-      st.clip_frac = n_eff ? (float)(a[4] / n_eff) : 0.0f;
+      st.entropy_mean = n_eff ? (float)(t[2] / n_eff) : 0.0f;
+      st.ratio_mean = n_eff ? (float)(t[3] / n_eff) : 0.0f;
+      st.clip_frac = n_eff ? (float)(t[4] / n_eff) : 0.0f;
+      st.kl_mean = n_eff ? (float)(t[5] / n_eff) : 0.0f;
+      st.tis_mean = n_eff ? (float)(t[6] / n_eff) : 1.0f;
       st.n_groups = Q;
       st.n_valid_rollouts = p.hdr->n_valid;
       st.n_policy_tokens = n_eff;

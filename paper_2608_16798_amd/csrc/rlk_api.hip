@@ -15,6 +15,11 @@
 
 namespace rlk {
 
+// Layouts the Python binding mirrors.
+static_assert(sizeof(rlk_batch_t) == 32, "rlk_batch_t layout");
+static_assert(sizeof(rlk_pg_params_t) == 72, "rlk_pg_params_t layout");
+static_assert(sizeof(rlk_pg_stats_t) == 48, "rlk_pg_stats_t layout");
+
 namespace {
 
 thread_local std::string g_last_error;
@@ -116,7 +121,7 @@ rlk_status_t layout(const rlk_batch_t* b, bool bwd, int64_t chunk_rows, WsLayout
   L.gsig = a.take((size_t)R * 8);
   L.geq = a.take((size_t)R * 4);
   L.adv = a.take((size_t)R * 4);
-  L.rsum = a.take((size_t)R * 32);
+  L.rsum = a.take((size_t)R * 8 * kRollSums);
   L.pm = a.take((size_t)L.nvt * Mc * 4);
   L.ps = a.take((size_t)L.nvt * Mc * 4);
   L.pu = a.take((size_t)L.nvt * Mc * 4);
@@ -384,8 +389,11 @@ rlk_status_t rlk_pg_loss_fwd_bwd(const rlk_batch_t* b, const void* hidden, const
   if (p->accumulate_dW != 0 && p->accumulate_dW != 1) return fail(RLK_EINVAL, "accumulate_dW must be 0 or 1");
   if (!(p->norm_override >= 0.0) || !isfinite(p->norm_override))
     return fail(RLK_EINVAL, "norm_override must be finite and >= 0");
-  for (int i = 0; i < 4; ++i)
-    if (p->reserved[i] != 0) return fail(RLK_EINVAL, "reserved parameter fields must be 0");
+  if (p->reserved != 0) return fail(RLK_EINVAL, "reserved parameter field must be 0");
+  if (p->rollout_logp ? !(p->tis_cap > 0.0f && isfinite(p->tis_cap)) : p->tis_cap != 0.0f)
+    return fail(RLK_EINVAL, "tis_cap must be finite and > 0 with rollout_logp, and 0 without");
+  if (!(p->kl_coef >= 0.0f) || !isfinite(p->kl_coef)) return fail(RLK_EINVAL, "kl_coef must be finite and >= 0");
+  if (p->kl_coef > 0.0f && !p->ref_logp) return fail(RLK_EINVAL, "kl_coef > 0 needs ref_logp");
   WsLayout L;
   st = layout(b, true, p->chunk_rows, L);
   if (st) return st;
@@ -461,6 +469,10 @@ rlk_status_t rlk_pg_loss_fwd_bwd(const rlk_batch_t* b, const void* hidden, const
     tp.ent_coef = p->entropy_coef;
     tp.agg = p->agg;
     tp.norm_override = p->norm_override;
+    tp.rollout_logp = p->rollout_logp;
+    tp.tis_cap = p->tis_cap;
+    tp.ref_logp = p->kl_coef > 0.0f ? p->ref_logp : nullptr;
+    tp.kl_coef = p->kl_coef;
     RLK_TRY(launch_combine(tp, s), "combine");
 
     DzParams dp = {};
@@ -532,6 +544,10 @@ rlk_status_t rlk_pg_loss_fwd_bwd(const rlk_batch_t* b, const void* hidden, const
   lp.ent_coef = p->entropy_coef;
   lp.agg = p->agg;
   lp.norm_override = p->norm_override;
+  lp.rollout_logp = p->rollout_logp;
+  lp.tis_cap = p->tis_cap;
+  lp.ref_logp = p->kl_coef > 0.0f ? p->ref_logp : nullptr;
+  lp.kl_coef = p->kl_coef;
   lp.loss = loss;
   lp.stats = stats;
   RLK_TRY(launch_loss(lp, s, 0), "loss");

@@ -27,6 +27,7 @@ constexpr int kChunkAlign = 256; // chunk_rows granularity
 constexpr int kKAlign = 64;      // K padding of the chunk buffers (bf16 elements per stage)
 constexpr int kScanTile = 4096;  // tokens per compaction block
 constexpr int kMaxRollouts = 16384;
+constexpr int kRollSums = 8;     // per-rollout fp64 sums of the loss reduction
 
 enum KernelKind {
   KK_BEGIN = 0,
@@ -69,7 +70,7 @@ struct WsLayout {
   size_t blkcnt = 0, blkoff = 0;
   // rollouts [R]
   size_t rstart = 0, rnpol = 0, first = 0, gidx = 0, gsize = 0, gmu = 0, gsig = 0, geq = 0, adv = 0;
-  size_t rsum = 0;  // double [R][4]
+  size_t rsum = 0;  // double [R][kRollSums]
   // chunk buffers
   size_t pm = 0, ps = 0, pu = 0;   // float [nvt][Mc]
   size_t hc = 0;                   // T [Mc][d]
@@ -113,6 +114,10 @@ struct TokenParams {
   float eps_low, eps_high, ent_coef;
   int agg;
   double norm_override;
+  const float* rollout_logp;   // truncated importance sampling (NULL = off)
+  float tis_cap;
+  const float* ref_logp;       // KL term (NULL = off)
+  float kl_coef;
 };
 hipError_t launch_combine(const TokenParams& p, hipStream_t s);
 
@@ -137,6 +142,10 @@ struct LossParams {
   float eps_low, eps_high, ent_coef;
   int agg;
   double norm_override;
+  const float* rollout_logp;
+  float tis_cap;
+  const float* ref_logp;
+  float kl_coef;
   float* loss;
   rlk_pg_stats_t* stats;
 };

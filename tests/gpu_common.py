@@ -71,7 +71,20 @@ def params_for(cfg, **kw):
     return rlk.make_params(**base)
 
 
-def run_gpu(inst, params, *, gid=None, mask="default", dW=None, ws=None):
+def aux_logps(inst, *, rollout_sigma=0.15, ref_sigma=0.3):
+    """Seeded rollout / reference log-probs of the instance's sampled tokens (host and device)."""
+    import torch
+
+    st = inst["st"]
+    seed = inst["cfg"].seed
+    ro = WL.perturbed_logps(inst["old_host"], st, rollout_sigma, seed + 7001)
+    rf = WL.perturbed_logps(inst["old_host"], st, ref_sigma, seed + 7002)
+    dev = inst["h"].device
+    return dict(rollout_host=ro, ref_host=rf, rollout=torch.as_tensor(ro, device=dev),
+                ref=torch.as_tensor(rf, device=dev))
+
+
+def run_gpu(inst, params, *, gid=None, mask="default", dW=None, ws=None, aux=None):
     import torch
 
     h, W = inst["h"], inst["W"]
@@ -82,20 +95,25 @@ def run_gpu(inst, params, *, gid=None, mask="default", dW=None, ws=None):
     loss, dh, dWo, ws = rlk.pg_loss_fwd_bwd(
         h, W, inst["targets"], inst["mask"] if mask == "default" else mask, inst["cu"], inst["old"],
         inst["rewards"], inst["gid"] if gid is None else gid, params, dW=dW, logp_out=logp, entropy_out=ent,
-        stats=stats, ws=ws)
+        stats=stats, ws=ws, rollout_logp=aux["rollout"] if aux else None, ref_logp=aux["ref"] if aux else None)
     torch.cuda.synchronize()
     flags = rlk.check_status(ws)
     return dict(loss=float(loss.item()), dh=dh, dW=dWo, logp=logp, ent=ent, stats=rlk.stats_from_tensor(stats),
                 flags=flags, ws=ws)
 
 
-def run_oracle(inst, params, *, grads=True):
+def run_oracle(inst, params, *, grads=True, aux=None):
     st = inst["st"]
+    extra = {}
+    if aux is not None and params.tis_cap > 0:
+        extra.update(rollout_logp=aux["rollout_host"], tis_cap=params.tis_cap)
+    if aux is not None and params.kl_coef > 0:
+        extra.update(ref_logp=aux["ref_host"], kl_coef=params.kl_coef)
     return O.pg_loss_fwd_bwd(
         to_host(inst["h"]), to_host(inst["W"]), st.targets, st.mask, st.cu_seqlens, inst["old_host"],
         st.rewards, st.group_ids, eps_low=params.eps_low, eps_high=params.eps_high, adv_eps=params.adv_eps,
         entropy_coef=params.entropy_coef, agg=params.agg,
-        norm_override=params.norm_override if params.norm_override > 0 else None, grads=grads)
+        norm_override=params.norm_override if params.norm_override > 0 else None, grads=grads, **extra)
 
 
 def rel_fro(a, b):
@@ -106,12 +124,12 @@ def rel_fro(a, b):
 
 
 def loss_scale(ref, params):
-    """L1 size of the loss terms: sum_t |w_t (s_t + c H_t)|."""
+    """L1 size of the loss terms: sum_t |omega_t w_t (s_t + c H_t - beta KL_t)|."""
     A = ref["adv"][ref["tok_rollout"]]
     rho = ref["rho"]
     c = np.clip(rho, 1 - params.eps_low, 1 + params.eps_high)
-    sv = np.minimum(rho * A, c * A) + params.entropy_coef * ref["H"]
-    return float(np.abs(ref["omega"] * sv).sum())
+    sv = np.minimum(rho * A, c * A) + params.entropy_coef * ref["H"] - params.kl_coef * ref["kl"]
+    return float(np.abs(ref["omega"] * ref["tis"] * sv).sum())
 
 
 def compare_full(inst, gpu, ref, params, tag=""):
@@ -139,6 +157,8 @@ def compare_full(inst, gpu, ref, params, tag=""):
     m["stats_ok"] = (st["n_policy_tokens"] == ref["stats"]["n_policy_tokens"]
                      and st["n_groups"] == ref["stats"]["n_groups"]
                      and st["n_valid_rollouts"] == ref["stats"]["n_valid_rollouts"])
+    m["kl_mean_err"] = abs(st["kl_mean"] - ref["stats"]["kl_mean"]) / max(1.0, abs(ref["stats"]["kl_mean"]))
+    m["tis_mean_err"] = abs(st["tis_mean"] - ref["stats"]["tis_mean"])
     m["flags"] = gpu["flags"]
     log(f"[{tag}] {cfg.name}: " + ", ".join(f"{k}={v:.3g}" if isinstance(v, float) else f"{k}={v}"
                                             for k, v in m.items()))
@@ -149,4 +169,5 @@ def compare_full(inst, gpu, ref, params, tag=""):
     assert m["loss_rel_l1"] <= TOL_LOSS
     assert m["dh_rel"] <= TOL_GRAD and m["dW_rel"] <= TOL_GRAD
     assert m["stats_ok"]
+    assert m["kl_mean_err"] <= 1e-3 and m["tis_mean_err"] <= 1e-4
     return m

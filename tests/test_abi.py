@@ -37,7 +37,7 @@ def test_exports_every_declared_symbol(lib):
 
 
 def test_version_and_strings(lib):
-    assert lib.rlk_version() == 1
+    assert lib.rlk_version() == 2
     assert lib.rlk_status_string(rlk.RLK_EWORKSPACE).decode().startswith("workspace")
     assert lib.rlk_kernel_kind_name(10).decode() == "fwd_lse_gemm"
 
@@ -98,8 +98,17 @@ def test_host_validation(lib):
         p = rlk.make_params(**kw)
         assert lib.rlk_pg_loss_fwd_bwd(*args(p)) == rlk.RLK_EINVAL, kw
     p = rlk.make_params()
-    p.reserved[2] = 1
+    p.reserved = 1
     assert lib.rlk_pg_loss_fwd_bwd(*args(p)) == rlk.RLK_EINVAL
+    # truncated importance sampling and the KL term
+    for kw, ro, rf in ((dict(tis_cap=1.5), None, None), (dict(), fake, None), (dict(tis_cap=-1.0), fake, None),
+                       (dict(tis_cap=float("inf")), fake, None), (dict(kl_coef=0.1), None, None),
+                       (dict(kl_coef=-0.1), None, fake), (dict(kl_coef=float("nan")), None, fake)):
+        p = rlk.make_params(**kw)
+        p.rollout_logp = ro
+        p.ref_logp = rf
+        assert lib.rlk_pg_loss_fwd_bwd(*args(p)) == rlk.RLK_EINVAL, (kw, ro, rf)
+    assert ctypes.sizeof(rlk.PgParams) == 72 and ctypes.sizeof(rlk.PgStats) == 48
     p = rlk.make_params()
     p.accumulate_dW = 2
     assert lib.rlk_pg_loss_fwd_bwd(*args(p)) == rlk.RLK_EINVAL

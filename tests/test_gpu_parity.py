@@ -9,7 +9,7 @@ that the oracle computes one by one and on properties that hold at any size.
 import numpy as np
 import pytest
 
-from gpu_common import (TOL_GRAD, TOL_LOGP, O, WL, build_instance, compare_full, ensure_library, log,
+from gpu_common import (TOL_GRAD, aux_logps, TOL_LOGP, O, WL, build_instance, compare_full, ensure_library, log,
                         params_for, rel_fro, rlk, run_gpu, run_oracle, to_host)
 
 pytestmark = pytest.mark.gpu
@@ -156,6 +156,22 @@ def test_pg_loss_parity(name, scaled, chunk):
     gpu = run_gpu(inst, p)
     ref = run_oracle(inst, p)
     compare_full(inst, gpu, ref, p, tag="seq")
+
+
+@pytest.mark.parametrize("name,scaled,agg", [("tiny_fp32", False, rlk.AGG_SEQ), ("small_bf16", True, rlk.AGG_SEQ),
+                                             ("qwen8b_bf16", True, rlk.AGG_TOKEN)])
+def test_pg_loss_tis_and_kl_parity(name, scaled, agg):
+    """Truncated importance sampling (Sec. 3.2.4) and the KL term (Sec. 2.3.2), both on, the cap
+    binding on part of the tokens."""
+    cfg = WL.scaled_config(name) if scaled else WL.get_config(name)
+    inst = build_instance(cfg)
+    aux = aux_logps(inst)
+    p = params_for(cfg, agg=agg, tis_cap=1.1, kl_coef=0.05, entropy_coef=0.01, chunk_rows=256 if scaled else 0)
+    log(f"pg_loss tis+kl {cfg.name} N={inst['st'].N}")
+    gpu = run_gpu(inst, p, aux=aux)
+    ref = run_oracle(inst, p, aux=aux)
+    assert 0 < np.mean(ref["tis"] == np.float64(p.tis_cap)) < 1
+    compare_full(inst, gpu, ref, p, tag="tis+kl")
 
 
 def test_pg_loss_token_mean_and_override():
