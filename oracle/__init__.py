@@ -17,4 +17,6 @@ from .rl_oracle import (  # noqa: F401
     kl_sampled,
     pg_loss_fwd_bwd,
     sampled_rows,
+    gae,
+    value_loss,
 )

@@ -38,6 +38,10 @@ Readings where the paper is silent (each one is stated where it is applied):
     default); when on, D_KL(pi_theta || pi_ref) at a sampled token is the
     estimator r/p - log(r/p) - 1 of the GRPO work the paper builds on, from the
     reference policy's log-prob of the sampled token (no second LM head);
+  * PPO (Sec. 2.3.1, simplified per Sec. 3.2.3): GAE runs over a rollout's policy
+    tokens in order (tool tokens stepped over), the terminal reward arriving at the
+    last policy token; a packed rollout is one trajectory; the value loss is the
+    token mean of (V - G)^2 over policy tokens, G = A + V;
   * token-level truncated importance sampling (Sec. 3.2.4) is optional (off by
     default); when on, w_t = min(exp(old_t - rollout_t), c_bar) scales the whole
     loss of token t (surrogate, entropy and KL terms) and is held constant in
@@ -232,13 +236,14 @@ def _aggregate(val, tok_rollout, n_pol, gi, G, n_groups, R, agg, norm_override):
 def pg_loss_fwd_bwd(h, W, targets, mask, cu_seqlens, old_logp, rewards, group_ids, *,
                     eps_low=0.2, eps_high=0.2, adv_eps=1e-6, entropy_coef=0.0, agg=AGG_SEQ,
                     norm_override=None, rollout_logp=None, tis_cap=None, ref_logp=None, kl_coef=0.0,
-                    grads=True, block: int = 128):
+                    token_adv=None, grads=True, block: int = 128):
     """Loss, per-token outputs and gradients w.r.t. hidden states and the LM-head weight.
 
     h [N, d], W [V, d] (any float dtype, evaluated in fp64), targets [N], mask [N]
     (None = all policy), cu_seqlens [R+1], old_logp [N], rewards [R], group_ids [R];
     rollout_logp [N] with tis_cap switches on truncated importance sampling, ref_logp [N]
-    with kl_coef > 0 the KL term.
+    with kl_coef > 0 the KL term; token_adv [N] (PPO, Sec. 2.3.1) replaces the group advantage
+    of each token by a per-token advantage.
     """
     h = np.asarray(h)
     W64 = _f64(W)
@@ -254,6 +259,7 @@ def pg_loss_fwd_bwd(h, W, targets, mask, cu_seqlens, old_logp, rewards, group_id
     n = idx.shape[0]
     omega = token_weights(tok_r, n_pol, gi, G, Q, agg, norm_override)
     tis = tis_weight(old[idx], _f64(rollout_logp)[idx], tis_cap) if rollout_logp is not None else np.ones(n)
+    adv_tok = _f64(token_adv)[idx] if token_adv is not None else adv[tok_r]
     ref = _f64(ref_logp)[idx] if (ref_logp is not None and kl_coef) else None
 
     lse = np.zeros(n)
@@ -281,7 +287,7 @@ def pg_loss_fwd_bwd(h, W, targets, mask, cu_seqlens, old_logp, rewards, group_id
         lse[b0:b1] = l
         logp[b0:b1] = lp[ar, yb]
         H[b0:b1] = -(p * lp).sum(axis=1)
-        sb, rb, cb = surrogate(logp[b0:b1], old[rows], adv[tok_r[b0:b1]], eps_low, eps_high)
+        sb, rb, cb = surrogate(logp[b0:b1], old[rows], adv_tok[b0:b1], eps_low, eps_high)
         s[b0:b1], rho[b0:b1], clipped[b0:b1] = sb, rb, cb
         # chain rule (w = tis weight, constant): dL/dlogp_t = omega_t w_t (A rho_t [not clipped]
         # - beta dKL_t/dlogp_t); dL/dH_t = omega_t w_t c_ent
@@ -289,7 +295,7 @@ def pg_loss_fwd_bwd(h, W, targets, mask, cu_seqlens, old_logp, rewards, group_id
         if ref is not None:
             kl[b0:b1], dkl = kl_sampled(logp[b0:b1], ref[b0:b1])
         wb = omega[b0:b1] * tis[b0:b1]
-        gb = wb * (adv[tok_r[b0:b1]] * rb * (~cb) - kl_coef * dkl)
+        gb = wb * (adv_tok[b0:b1] * rb * (~cb) - kl_coef * dkl)
         eb = wb * entropy_coef
         g[b0:b1], e[b0:b1] = gb, eb
         if grads:
@@ -319,7 +325,7 @@ def pg_loss_fwd_bwd(h, W, targets, mask, cu_seqlens, old_logp, rewards, group_id
     lse_full[idx] = lse
     return dict(loss=-J, pg_loss=-Jpg, stats=stats, idx=idx, tok_rollout=tok_r, n_pol=n_pol,
                 adv=adv, group_index=gi, n_groups=Q, omega=omega, lse=lse, logp=logp, H=H,
-                rho=rho, clipped=clipped, kl=kl, tis=tis, g=g, e=e, logp_full=logp_full, entropy_full=H_full,
+                rho=rho, clipped=clipped, kl=kl, tis=tis, adv_tok=adv_tok, g=g, e=e, logp_full=logp_full, entropy_full=H_full,
                 lse_full=lse_full, dh=dh, dW=dW)
 
 
@@ -368,3 +374,53 @@ def sampled_rows(h_rows, W, y_rows, old_rows, adv_rows, omega_rows, *, eps_low, 
         out["e"][b0:b1] = eb
         out["dh"][b0:b1] = dz @ W64
     return out
+
+
+# --------------------------------------------------------------------------
+# PPO path (Sec. 2.3.1 GAE and value loss; Sec. 3.2.3 simplified variant).
+# --------------------------------------------------------------------------
+def gae(values, rewards, mask, cu_seqlens, group_ids=None, gamma=1.0, lam=1.0):
+    """Masked generalised advantage estimation per rollout, and the returns.
+
+    Sec. 2.3.1: A_t = sum_l (gamma lam)^l delta_{t+l} M_{t+l}, delta_t = r_t + gamma V(s_{t+1})
+    M_{t+1} - V(s_t); Sec. 3.2.3: the rollout's terminal reward R_i is received at its final
+    token.  Reading: the recursion runs over the rollout's policy tokens (M = 1) in order, the
+    state after a policy token being the next policy token of the rollout (tool tokens carry no
+    value and are stepped over), and the reward arrives at the last policy token; with
+    gamma = lam = 1 this gives A_t = R_i - V(s_t), the form Sec. 3.2.3 states.  Returns
+    G_t = A_t + V(s_t).  Masked rows and rows of excluded rollouts (group id < 0) are 0.
+    """
+    V = _f64(values)
+    mask = np.asarray(mask).astype(bool)
+    cu = np.asarray(cu_seqlens, dtype=np.int64)
+    R = cu.shape[0] - 1
+    gid = np.zeros(R, dtype=np.int64) if group_ids is None else np.asarray(group_ids, dtype=np.int64)
+    adv = np.zeros(V.shape[0])
+    ret = np.zeros(V.shape[0])
+    for r in range(R):
+        if gid[r] < 0:
+            continue
+        pos = [t for t in range(cu[r], cu[r + 1]) if mask[t]]
+        a_next, v_next = 0.0, 0.0
+        for j in range(len(pos) - 1, -1, -1):
+            t = pos[j]
+            last = j == len(pos) - 1
+            delta = (float(rewards[r]) if last else 0.0) + (0.0 if last else gamma * v_next) - V[t]
+            a = delta + gamma * lam * a_next
+            adv[t], ret[t] = a, a + V[t]
+            a_next, v_next = a, V[t]
+    return adv, ret
+
+
+def value_loss(values, returns, mask, cu_seqlens, group_ids=None):
+    """Sec. 2.3.1 masked mean-squared value loss E_t[M_t (V(s_t) - G_t)^2] (token mean over the
+    policy tokens of non-excluded rollouts) and its gradient with respect to V."""
+    V = _f64(values)
+    G = _f64(returns)
+    idx, _, _ = compact(mask, cu_seqlens, group_ids)
+    dV = np.zeros(V.shape[0])
+    if idx.size == 0:
+        return 0.0, dV
+    diff = V[idx] - G[idx]
+    dV[idx] = 2.0 * diff / idx.size
+    return float((diff * diff).mean()), dV

@@ -501,3 +501,115 @@ def test_tis_and_kl_gradients_match_finite_differences(agg):
             lm_ = _loss(bp, grads=False, **kw)["loss"]
             fd = (lp_ - lm_) / (2 * step)
             assert abs(fd - grad[ij]) <= 1e-6 * max(1.0, abs(grad).max()), (name, ij, fd, grad[ij])
+
+
+# ------------------------------------------------ PPO path: GAE, value loss, token advantages
+def _gae_case(seed=40, R=4):
+    rng = np.random.default_rng(seed)
+    lens = rng.integers(5, 14, size=R)
+    cu = np.concatenate([[0], np.cumsum(lens)])
+    N = int(cu[-1])
+    mask = (rng.random(N) > 0.35).astype(np.uint8)
+    values = rng.standard_normal(N)
+    rewards = rng.random(R)
+    return dict(values=values, rewards=rewards, mask=mask, cu=cu)
+
+
+def test_gae_gamma_lambda_one_is_reward_minus_value():
+    # Sec. 3.2.3: with gamma = lambda = 1 the recursion degenerates to A_t = R_i - V(s_t)
+    c = _gae_case()
+    adv, ret = O.gae(c["values"], c["rewards"], c["mask"], c["cu"], None, 1.0, 1.0)
+    for r in range(len(c["rewards"])):
+        for t in range(c["cu"][r], c["cu"][r + 1]):
+            if c["mask"][t]:
+                np.testing.assert_allclose(adv[t], c["rewards"][r] - c["values"][t], rtol=0, atol=1e-12)
+                np.testing.assert_allclose(ret[t], c["rewards"][r], rtol=0, atol=1e-12)
+            else:
+                assert adv[t] == 0 and ret[t] == 0
+
+
+def _policy_seq(c, r):
+    return [t for t in range(c["cu"][r], c["cu"][r + 1]) if c["mask"][t]]
+
+
+@pytest.mark.parametrize("gamma,lam", [(0.9, 0.0), (0.97, 0.8), (1.0, 0.5), (0.5, 1.0)])
+def test_gae_is_the_discounted_sum_of_td_residuals(gamma, lam):
+    # brute force on the definition: A_t = sum_l (gamma lam)^l delta_{t+l}, delta from next policy token
+    c = _gae_case(41)
+    adv, ret = O.gae(c["values"], c["rewards"], c["mask"], c["cu"], None, gamma, lam)
+    V = c["values"]
+    for r in range(len(c["rewards"])):
+        pos = _policy_seq(c, r)
+        deltas = []
+        for j, t in enumerate(pos):
+            nxt = gamma * V[pos[j + 1]] if j + 1 < len(pos) else c["rewards"][r]
+            deltas.append(nxt - V[t])
+        for j, t in enumerate(pos):
+            want = sum((gamma * lam) ** l * deltas[j + l] for l in range(len(pos) - j))
+            np.testing.assert_allclose(adv[t], want, rtol=1e-12, atol=1e-12)
+            np.testing.assert_allclose(ret[t], want + V[t], rtol=1e-12, atol=1e-12)
+        if lam == 0.0:   # one-step residuals
+            np.testing.assert_allclose(adv[pos], deltas, rtol=1e-12, atol=1e-12)
+
+
+def test_gae_steps_over_tool_tokens_and_skips_excluded_rollouts():
+    c = _gae_case(42)
+    adv, _ = O.gae(c["values"], c["rewards"], c["mask"], c["cu"], None, 0.95, 0.9)
+    # drop every tool token: the policy tokens' advantages are unchanged
+    keep = c["mask"].astype(bool)
+    cu2 = np.concatenate([[0], np.cumsum([keep[c["cu"][r]:c["cu"][r + 1]].sum() for r in range(len(c["rewards"]))])])
+    adv2, _ = O.gae(c["values"][keep], c["rewards"], np.ones(keep.sum(), np.uint8), cu2, None, 0.95, 0.9)
+    np.testing.assert_allclose(adv[keep], adv2, rtol=1e-12, atol=1e-14)
+    gid = np.array([3, -1, 3, 5])
+    adv3, ret3 = O.gae(c["values"], c["rewards"], c["mask"], c["cu"], gid, 0.95, 0.9)
+    ex = slice(c["cu"][1], c["cu"][2])
+    assert np.all(adv3[ex] == 0) and np.all(ret3[ex] == 0)
+    np.testing.assert_array_equal(adv3[:c["cu"][1]], adv[:c["cu"][1]])
+
+
+def test_value_loss_closed_form_and_finite_differences():
+    c = _gae_case(43)
+    G = np.random.default_rng(44).standard_normal(c["values"].shape)
+    loss, dV = O.value_loss(c["values"], G, c["mask"], c["cu"])
+    m = c["mask"].astype(bool)
+    np.testing.assert_allclose(loss, np.mean((c["values"][m] - G[m]) ** 2), rtol=1e-12)
+    assert np.all(dV[~m] == 0)
+    for t in np.flatnonzero(m)[:10]:
+        vp = c["values"].copy()
+        vp[t] += 1e-6
+        lp_, _ = O.value_loss(vp, G, c["mask"], c["cu"])
+        vp[t] -= 2e-6
+        lm_, _ = O.value_loss(vp, G, c["mask"], c["cu"])
+        np.testing.assert_allclose((lp_ - lm_) / 2e-6, dV[t], rtol=1e-6, atol=1e-10)
+
+
+def test_token_advantages_reduce_to_the_group_advantages():
+    b = _with_old_from_current(45, excluded=(2,))
+    kw = dict(eps_low=0.2, eps_high=0.28, entropy_coef=0.02)
+    grpo = _loss(b, **kw)
+    tok = np.zeros(b["h"].shape[0])
+    tok[grpo["idx"]] = grpo["adv"][grpo["tok_rollout"]]
+    ppo = _loss(b, token_adv=tok, **kw)
+    assert ppo["loss"] == grpo["loss"]
+    np.testing.assert_array_equal(ppo["dh"], grpo["dh"])
+    np.testing.assert_array_equal(ppo["dW"], grpo["dW"])
+
+
+def test_token_advantage_gradients_match_finite_differences():
+    b = _with_old_from_current(47, excluded=(1,), sigma=0.6)
+    b = _kink_safe(b, 0.2, 0.2)
+    tok = np.random.default_rng(47).standard_normal(b["h"].shape[0])
+    kw = dict(eps_low=0.2, eps_high=0.2, agg=O.AGG_TOKEN, token_adv=tok)
+    out = _loss(b, **kw)
+    assert 0 < out["stats"]["clip_frac"] < 1
+    rng = np.random.default_rng(48)
+    for name, grad in (("h", out["dh"]), ("W", out["dW"])):
+        X = b[name]
+        for ij in [tuple(rng.integers(0, s) for s in X.shape) for _ in range(15)]:
+            bp = dict(b)
+            bp[name] = X.copy()
+            bp[name][ij] += 1e-6
+            lp_ = _loss(bp, grads=False, **kw)["loss"]
+            bp[name][ij] -= 2e-6
+            lm_ = _loss(bp, grads=False, **kw)["loss"]
+            assert abs((lp_ - lm_) / 2e-6 - grad[ij]) <= 1e-6 * max(1.0, abs(grad).max())
