@@ -106,7 +106,10 @@ typedef struct {
   const float* ref_logp;
   float tis_cap;
   float kl_coef;
-  int64_t reserved;     /* must be 0 */
+  /* PPO (Sec. 2.3.1): device [N] f32 per-token advantages (e.g. from rlk_gae) used in place of
+   * the group advantages; NULL = group advantages (GRPO).  Rewards and group ids still define
+   * exclusion and the SEQ aggregation. */
+  const float* token_adv;
 } rlk_pg_params_t;
 
 typedef struct {
@@ -179,6 +182,30 @@ rlk_status_t rlk_pg_loss_fwd_bwd(const rlk_batch_t* b, const void* hidden, const
                                  float* loss, void* dhidden, float* dW, float* logp_out,
                                  float* entropy_out, rlk_pg_stats_t* stats, void* ws,
                                  size_t ws_bytes, void* stream);
+
+/* Masked generalised advantage estimation (Sec. 2.3.1 GAE equation; Sec. 3.2.3: the rollout's
+ * terminal reward arrives at its final token, gamma = lambda = 1 giving A_t = R_i - V(s_t)).
+ * Per rollout r (rows cu_seqlens[r] .. cu_seqlens[r+1] - 1 of the packed batch, one trajectory):
+ * over its policy rows (mask 1) in order, delta_t = gamma V[next] - V[t] with next the following
+ * policy row of the rollout, or rewards[r] - V[t] at the last one; adv[t] = sum_l (gamma
+ * lam)^l delta_{t+l}; returns[t] = adv[t] + V[t].  Tool rows (mask 0) are stepped over and
+ * written as 0, as are the rows of excluded rollouts (group_ids[r] < 0; group_ids may be NULL).
+ * Device pointers: mask [N], values [N] f32, rewards [R] f32, adv and returns [N] f32 (returns
+ * may be NULL).  cu_seqlens [R+1] device; entries are clamped to [0, N] (no error is raised).
+ * Uses no workspace. */
+rlk_status_t rlk_gae(int64_t N, int32_t R, const int32_t* cu_seqlens, const uint8_t* mask,
+                     const float* values, const float* rewards, const int32_t* group_ids, float gamma,
+                     float lam, float* adv, float* returns, void* stream);
+
+/* Masked mean-squared value loss (Sec. 2.3.1): loss = mean over the policy rows of non-excluded
+ * rollouts of (values[t] - returns[t])^2 (0 when there is none); dvalues[t] = dloss/dvalues[t]
+ * = 2 (values[t] - returns[t]) / count on those rows, 0 elsewhere (dvalues may be NULL).
+ * Device pointers as in rlk_gae; loss device float[1].  ws: rlk_value_workspace_size bytes,
+ * 256-byte aligned, deterministic reduction (per-rollout fp64 partial sums). */
+rlk_status_t rlk_value_workspace_size(int32_t R, size_t* bytes);
+rlk_status_t rlk_value_loss(int64_t N, int32_t R, const int32_t* cu_seqlens, const uint8_t* mask,
+                            const float* values, const float* returns, const int32_t* group_ids, float* loss,
+                            float* dvalues, void* ws, size_t ws_bytes, void* stream);
 
 /* Synchronises `stream`, then reads the status word that the previous calls using `ws`
  * left there.  *flags (optional host pointer) receives RLK_DERR_* bits; returns RLK_OK or

@@ -22,7 +22,8 @@ DERR_TARGET, DERR_CU_SEQLENS = 1, 2
 EXPORTS = [
     "rlk_workspace_size", "rlk_advantage_workspace_size", "rlk_compact", "rlk_logprob_fwd", "rlk_group_advantage",
     "rlk_pg_loss_fwd_bwd", "rlk_check_status", "rlk_status_string", "rlk_last_error", "rlk_version",
-    "rlk_profile_begin", "rlk_profile_end", "rlk_kernel_kind_name",
+    "rlk_profile_begin", "rlk_profile_end", "rlk_kernel_kind_name", "rlk_gae", "rlk_value_workspace_size",
+    "rlk_value_loss",
 ]
 
 
@@ -36,7 +37,7 @@ class PgParams(ctypes.Structure):
                 ("entropy_coef", ctypes.c_float), ("agg", ctypes.c_int32), ("accumulate_dW", ctypes.c_int32),
                 ("norm_override", ctypes.c_double), ("chunk_rows", ctypes.c_int64),
                 ("rollout_logp", ctypes.c_void_p), ("ref_logp", ctypes.c_void_p), ("tis_cap", ctypes.c_float),
-                ("kl_coef", ctypes.c_float), ("reserved", ctypes.c_int64)]
+                ("kl_coef", ctypes.c_float), ("token_adv", ctypes.c_void_p)]
 
 
 class PgStats(ctypes.Structure):
@@ -80,6 +81,10 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.rlk_profile_begin.argtypes = []
     lib.rlk_profile_end.argtypes = [i32, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(i32), ctypes.POINTER(i32)]
     lib.rlk_kernel_kind_name.argtypes = [i32]
+    i64 = ctypes.c_int64
+    lib.rlk_gae.argtypes = [i64, i32, vp, vp, vp, vp, vp, f32, f32, vp, vp, vp]
+    lib.rlk_value_workspace_size.argtypes = [i32, ctypes.POINTER(sz)]
+    lib.rlk_value_loss.argtypes = [i64, i32, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
     lib.rlk_kernel_kind_name.restype = ctypes.c_char_p
     for name in EXPORTS:
         if name not in ("rlk_status_string", "rlk_last_error", "rlk_kernel_kind_name", "rlk_version"):
@@ -219,17 +224,19 @@ def group_advantage(rewards, group_ids, adv_eps=1e-6, adv=None, group_index=None
 
 def pg_loss_fwd_bwd(hidden, W, targets, mask, cu_seqlens, old_logp, rewards, group_ids, params: PgParams,
                     loss=None, dhidden=None, dW=None, logp_out=None, entropy_out=None, stats=None, ws=None,
-                    stream=None, rollout_logp=None, ref_logp=None):
+                    stream=None, rollout_logp=None, ref_logp=None, token_adv=None):
     """Loss, dL/dhidden and dL/dW of the masked clipped policy-gradient objective.
     rollout_logp / ref_logp ([N] fp32 device tensors or None) feed truncated importance sampling
-    (params.tis_cap) and the KL term (params.kl_coef)."""
+    (params.tis_cap) and the KL term (params.kl_coef); token_adv ([N] fp32, e.g. from gae())
+    replaces the group advantages (PPO)."""
     import torch
 
     lib = load_library()
-    if rollout_logp is not None or ref_logp is not None:
+    if rollout_logp is not None or ref_logp is not None or token_adv is not None:
         params = PgParams.from_buffer_copy(bytes(params))
         params.rollout_logp = _ptr(rollout_logp)
         params.ref_logp = _ptr(ref_logp)
+        params.token_adv = _ptr(token_adv)
     b = make_batch(hidden, W, cu_seqlens)
     dev = hidden.device
     if loss is None:
@@ -245,6 +252,45 @@ def pg_loss_fwd_bwd(hidden, W, targets, mask, cu_seqlens, old_logp, rewards, gro
                                    _ptr(dhidden), _ptr(dW), _ptr(logp_out), _ptr(entropy_out), _ptr(stats),
                                    _ptr(ws), ws.numel(), _stream_handle(stream)))
     return loss, dhidden, dW, ws
+
+
+def gae(values, rewards, mask, cu_seqlens, group_ids=None, gamma=1.0, lam=1.0, adv=None, returns=None, stream=None):
+    """Masked GAE per rollout (see rlk_gae); returns (adv, returns) as [N] fp32 device tensors."""
+    import torch
+
+    lib = load_library()
+    N, R = values.shape[0], rewards.shape[0]
+    if adv is None:
+        adv = torch.empty(N, dtype=torch.float32, device=values.device)
+    if returns is None:
+        returns = torch.empty(N, dtype=torch.float32, device=values.device)
+    _check(lib.rlk_gae(N, R, _ptr(cu_seqlens), _ptr(mask), _ptr(values), _ptr(rewards), _ptr(group_ids),
+                       gamma, lam, _ptr(adv), _ptr(returns), _stream_handle(stream)))
+    return adv, returns
+
+
+def value_workspace_size(R: int) -> int:
+    n = ctypes.c_size_t()
+    _check(load_library().rlk_value_workspace_size(R, ctypes.byref(n)))
+    return n.value
+
+
+def value_loss(values, returns, mask, cu_seqlens, group_ids=None, loss=None, dvalues=None, ws=None, stream=None):
+    """Masked mean-squared value loss and its gradient (see rlk_value_loss)."""
+    import torch
+
+    lib = load_library()
+    N, R = values.shape[0], cu_seqlens.shape[0] - 1
+    dev = values.device
+    if loss is None:
+        loss = torch.empty(1, dtype=torch.float32, device=dev)
+    if dvalues is None:
+        dvalues = torch.empty(N, dtype=torch.float32, device=dev)
+    if ws is None:
+        ws = alloc_workspace(value_workspace_size(R), dev)
+    _check(lib.rlk_value_loss(N, R, _ptr(cu_seqlens), _ptr(mask), _ptr(values), _ptr(returns), _ptr(group_ids),
+                              _ptr(loss), _ptr(dvalues), _ptr(ws), ws.numel(), _stream_handle(stream)))
+    return loss, dvalues
 
 
 def check_status(ws, stream=None) -> int:

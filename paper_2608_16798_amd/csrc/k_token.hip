@@ -152,7 +152,7 @@ __global__ void __launch_bounds__(256) k_combine(TokenParams p) {
   if (p.lse_out) p.lse_out[row] = lsef;
   if (p.with_grad) {
     const int r = p.tokr[i];
-    const float A = p.adv[r];
+    const float A = p.token_adv ? p.token_adv[row] : p.adv[r];
     const float old = p.old_logp[row];
     const float rho = expf(logp - old);
     double w;
@@ -276,7 +276,7 @@ __global__ void __launch_bounds__(256) k_loss_rollout(LossParams p) {
   const int r = blockIdx.x;
   const int n = p.rnpol[r];
   const int s0 = p.rstart[r];
-  const float A = p.adv[r];
+  const float Ar = p.adv[r];
   double acc[kRollSums];
 #pragma unroll
   for (int f = 0; f < kRollSums; ++f) acc[f] = 0.0;
@@ -284,6 +284,7 @@ __global__ void __launch_bounds__(256) k_loss_rollout(LossParams p) {
     for (int k = threadIdx.x; k < n; k += 256) {
       const int i = s0 + k;
       const int64_t row = p.idx[i];
+      const float A = p.token_adv ? p.token_adv[row] : Ar;
       const float logp = p.logp[i];
       const float old = p.old_logp[row];
       const float rho = expf(logp - old);

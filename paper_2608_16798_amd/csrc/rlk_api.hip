@@ -195,7 +195,8 @@ Prof& prof() {
 const char* kKindNames[KK_COUNT_KINDS] = {
     "begin",        "compact_count", "compact_scan",  "compact_write", "rollout_offsets", "group_rank",
     "group_stats",  "advantage",     "transpose_w",   "gather",        "fwd_lse_gemm",    "lse_combine",
-    "dz",           "dh_gemm",       "dw_gemm",       "loss_rollout",  "loss_final",      "zero_fill"};
+    "dz",           "dh_gemm",       "dw_gemm",       "loss_rollout",  "loss_final",      "zero_fill",
+    "gae",          "value_loss"};
 
 }  // namespace
 
@@ -389,7 +390,6 @@ rlk_status_t rlk_pg_loss_fwd_bwd(const rlk_batch_t* b, const void* hidden, const
   if (p->accumulate_dW != 0 && p->accumulate_dW != 1) return fail(RLK_EINVAL, "accumulate_dW must be 0 or 1");
   if (!(p->norm_override >= 0.0) || !isfinite(p->norm_override))
     return fail(RLK_EINVAL, "norm_override must be finite and >= 0");
-  if (p->reserved != 0) return fail(RLK_EINVAL, "reserved parameter field must be 0");
   if (p->rollout_logp ? !(p->tis_cap > 0.0f && isfinite(p->tis_cap)) : p->tis_cap != 0.0f)
     return fail(RLK_EINVAL, "tis_cap must be finite and > 0 with rollout_logp, and 0 without");
   if (!(p->kl_coef >= 0.0f) || !isfinite(p->kl_coef)) return fail(RLK_EINVAL, "kl_coef must be finite and >= 0");
@@ -473,6 +473,7 @@ rlk_status_t rlk_pg_loss_fwd_bwd(const rlk_batch_t* b, const void* hidden, const
     tp.tis_cap = p->tis_cap;
     tp.ref_logp = p->kl_coef > 0.0f ? p->ref_logp : nullptr;
     tp.kl_coef = p->kl_coef;
+    tp.token_adv = p->token_adv;
     RLK_TRY(launch_combine(tp, s), "combine");
 
     DzParams dp = {};
@@ -548,6 +549,7 @@ rlk_status_t rlk_pg_loss_fwd_bwd(const rlk_batch_t* b, const void* hidden, const
   lp.tis_cap = p->tis_cap;
   lp.ref_logp = p->kl_coef > 0.0f ? p->ref_logp : nullptr;
   lp.kl_coef = p->kl_coef;
+  lp.token_adv = p->token_adv;
   lp.loss = loss;
   lp.stats = stats;
   RLK_TRY(launch_loss(lp, s, 0), "loss");
@@ -555,6 +557,54 @@ rlk_status_t rlk_pg_loss_fwd_bwd(const rlk_batch_t* b, const void* hidden, const
                            entropy_out, nullptr, s),
           "zero_fill");
   return finish(hipSuccess, "", ws, s);
+}
+
+rlk_status_t rlk_gae(int64_t N, int32_t R, const int32_t* cu_seqlens, const uint8_t* mask, const float* values,
+                     const float* rewards, const int32_t* group_ids, float gamma, float lam, float* adv,
+                     float* returns, void* stream) {
+  if (N < 0 || R < 0 || R > kMaxRollouts) return fail(RLK_ESHAPE, "N = %lld or R = %d out of range", (long long)N, R);
+  if (!(gamma >= 0.0f && gamma <= 1.0f) || !(lam >= 0.0f && lam <= 1.0f))
+    return fail(RLK_EINVAL, "gamma and lam must lie in [0, 1]");
+  if (R == 0) return RLK_OK;
+  if (!cu_seqlens || !rewards) return fail(RLK_EINVAL, "cu_seqlens or rewards is NULL");
+  if (N > 0 && (!mask || !values || !adv)) return fail(RLK_EINVAL, "mask, values or adv is NULL");
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  RLK_TRY(launch_gae(N, R, cu_seqlens, mask, values, rewards, group_ids, gamma, lam, adv, returns, s), "gae");
+  return RLK_OK;
+}
+
+rlk_status_t rlk_value_workspace_size(int32_t R, size_t* bytes) {
+  if (!bytes) return fail(RLK_EINVAL, "bytes is NULL");
+  if (R < 0 || R > kMaxRollouts) return fail(RLK_ESHAPE, "R = %d outside [0, %d]", R, kMaxRollouts);
+  Alloc a;
+  a.take(sizeof(WsHeader));
+  a.take(sizeof(double) * 2);
+  a.take((size_t)R * 16);
+  *bytes = a.off;
+  return RLK_OK;
+}
+
+rlk_status_t rlk_value_loss(int64_t N, int32_t R, const int32_t* cu_seqlens, const uint8_t* mask,
+                            const float* values, const float* returns, const int32_t* group_ids, float* loss,
+                            float* dvalues, void* ws, size_t ws_bytes, void* stream) {
+  if (N < 0 || R < 0 || R > kMaxRollouts) return fail(RLK_ESHAPE, "N = %lld or R = %d out of range", (long long)N, R);
+  if (!loss) return fail(RLK_EINVAL, "loss is NULL");
+  if (R > 0 && !cu_seqlens) return fail(RLK_EINVAL, "cu_seqlens is NULL");
+  if (N > 0 && (!mask || !values || !returns)) return fail(RLK_EINVAL, "mask, values or returns is NULL");
+  size_t need = 0;
+  rlk_status_t st = rlk_value_workspace_size(R, &need);
+  if (st) return st;
+  st = check_ws(ws, ws_bytes, need);
+  if (st) return st;
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  Alloc a;
+  char* w = static_cast<char*>(ws);
+  a.take(sizeof(WsHeader));
+  double* total = reinterpret_cast<double*>(w + a.take(sizeof(double) * 2));
+  double* part = reinterpret_cast<double*>(w + a.take((size_t)R * 16));
+  RLK_TRY(launch_value_loss(N, R, cu_seqlens, mask, values, returns, group_ids, part, total, loss, dvalues, s),
+          "value_loss");
+  return RLK_OK;
 }
 
 rlk_status_t rlk_check_status(const void* ws, void* stream, int32_t* flags) {

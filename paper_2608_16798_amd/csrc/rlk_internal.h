@@ -48,6 +48,8 @@ enum KernelKind {
   KK_LOSS_ROLLOUT,
   KK_LOSS_FINAL,
   KK_ZERO_FILL,
+  KK_GAE,
+  KK_VALUE_LOSS,
   KK_COUNT_KINDS
 };
 
@@ -118,6 +120,7 @@ struct TokenParams {
   float tis_cap;
   const float* ref_logp;       // KL term (NULL = off)
   float kl_coef;
+  const float* token_adv;      // per-token advantages (NULL = group advantages)
 };
 hipError_t launch_combine(const TokenParams& p, hipStream_t s);
 
@@ -146,6 +149,7 @@ struct LossParams {
   float tis_cap;
   const float* ref_logp;
   float kl_coef;
+  const float* token_adv;
   float* loss;
   rlk_pg_stats_t* stats;
 };
@@ -153,6 +157,14 @@ hipError_t launch_loss(const LossParams& p, hipStream_t s, int prof_kind_first);
 
 hipError_t launch_zero_fill(int dtype, const uint8_t* keep, int64_t N, int d, void* dh, float* o1, float* o2,
                             float* o3, hipStream_t s);
+
+// ---- launchers (k_ppo.hip) ----
+hipError_t launch_gae(int64_t N, int R, const int32_t* cu, const uint8_t* mask, const float* values,
+                      const float* rewards, const int32_t* gid, float gamma, float lam, float* adv, float* ret,
+                      hipStream_t s);
+hipError_t launch_value_loss(int64_t N, int R, const int32_t* cu, const uint8_t* mask, const float* values,
+                             const float* ret, const int32_t* gid, double* part, double* total, float* loss,
+                             float* dv, hipStream_t s);
 
 // ---- launchers (k_gemm.hip) ----
 struct GemmArgs {

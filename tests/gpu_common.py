@@ -84,7 +84,7 @@ def aux_logps(inst, *, rollout_sigma=0.15, ref_sigma=0.3):
                 ref=torch.as_tensor(rf, device=dev))
 
 
-def run_gpu(inst, params, *, gid=None, mask="default", dW=None, ws=None, aux=None):
+def run_gpu(inst, params, *, gid=None, mask="default", dW=None, ws=None, aux=None, token_adv=None):
     import torch
 
     h, W = inst["h"], inst["W"]
@@ -95,16 +95,17 @@ def run_gpu(inst, params, *, gid=None, mask="default", dW=None, ws=None, aux=Non
     loss, dh, dWo, ws = rlk.pg_loss_fwd_bwd(
         h, W, inst["targets"], inst["mask"] if mask == "default" else mask, inst["cu"], inst["old"],
         inst["rewards"], inst["gid"] if gid is None else gid, params, dW=dW, logp_out=logp, entropy_out=ent,
-        stats=stats, ws=ws, rollout_logp=aux["rollout"] if aux else None, ref_logp=aux["ref"] if aux else None)
+        stats=stats, ws=ws, rollout_logp=aux["rollout"] if aux else None, ref_logp=aux["ref"] if aux else None,
+        token_adv=token_adv)
     torch.cuda.synchronize()
     flags = rlk.check_status(ws)
     return dict(loss=float(loss.item()), dh=dh, dW=dWo, logp=logp, ent=ent, stats=rlk.stats_from_tensor(stats),
                 flags=flags, ws=ws)
 
 
-def run_oracle(inst, params, *, grads=True, aux=None):
+def run_oracle(inst, params, *, grads=True, aux=None, token_adv=None):
     st = inst["st"]
-    extra = {}
+    extra = {} if token_adv is None else dict(token_adv=token_adv)
     if aux is not None and params.tis_cap > 0:
         extra.update(rollout_logp=aux["rollout_host"], tis_cap=params.tis_cap)
     if aux is not None and params.kl_coef > 0:
@@ -125,7 +126,7 @@ def rel_fro(a, b):
 
 def loss_scale(ref, params):
     """L1 size of the loss terms: sum_t |omega_t w_t (s_t + c H_t - beta KL_t)|."""
-    A = ref["adv"][ref["tok_rollout"]]
+    A = ref["adv_tok"]
     rho = ref["rho"]
     c = np.clip(rho, 1 - params.eps_low, 1 + params.eps_high)
     sv = np.minimum(rho * A, c * A) + params.entropy_coef * ref["H"] - params.kl_coef * ref["kl"]

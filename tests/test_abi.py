@@ -97,9 +97,6 @@ def test_host_validation(lib):
     for kw in (dict(eps_low=1.0), dict(eps_low=-0.1), dict(agg=3), dict(adv_eps=-1.0)):
         p = rlk.make_params(**kw)
         assert lib.rlk_pg_loss_fwd_bwd(*args(p)) == rlk.RLK_EINVAL, kw
-    p = rlk.make_params()
-    p.reserved = 1
-    assert lib.rlk_pg_loss_fwd_bwd(*args(p)) == rlk.RLK_EINVAL
     # truncated importance sampling and the KL term
     for kw, ro, rf in ((dict(tis_cap=1.5), None, None), (dict(), fake, None), (dict(tis_cap=-1.0), fake, None),
                        (dict(tis_cap=float("inf")), fake, None), (dict(kl_coef=0.1), None, None),
@@ -109,6 +106,18 @@ def test_host_validation(lib):
         p.ref_logp = rf
         assert lib.rlk_pg_loss_fwd_bwd(*args(p)) == rlk.RLK_EINVAL, (kw, ro, rf)
     assert ctypes.sizeof(rlk.PgParams) == 72 and ctypes.sizeof(rlk.PgStats) == 48
+    # GAE / value loss
+    assert lib.rlk_gae(10, 2, fake, fake, fake, fake, None, ctypes.c_float(1.5), ctypes.c_float(1.0), fake, None,
+                       None) == rlk.RLK_EINVAL
+    assert lib.rlk_gae(10, 2, None, fake, fake, fake, None, ctypes.c_float(1.0), ctypes.c_float(1.0), fake, None,
+                       None) == rlk.RLK_EINVAL
+    assert lib.rlk_gae(-1, 2, fake, fake, fake, fake, None, ctypes.c_float(1.0), ctypes.c_float(1.0), fake, None,
+                       None) == rlk.RLK_ESHAPE
+    need = rlk.value_workspace_size(4)
+    assert need > 0
+    assert lib.rlk_value_loss(10, 4, fake, fake, fake, fake, None, fake, None, fake, need - 1, None) \
+        == rlk.RLK_EWORKSPACE
+    assert lib.rlk_value_loss(10, 4, fake, fake, fake, fake, None, None, None, fake, need, None) == rlk.RLK_EINVAL
     p = rlk.make_params()
     p.accumulate_dW = 2
     assert lib.rlk_pg_loss_fwd_bwd(*args(p)) == rlk.RLK_EINVAL

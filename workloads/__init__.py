@@ -11,7 +11,7 @@ and LM-head weights) come from torch's generator on the requested device.
 """
 from .configs import CONFIGS, Config, get_config, scaled_config
 from .gen import (Structure, make_structure, make_tensors, old_logp_from_anchor, perturbed_logps,
-                  sample_policy_rows)
+                  sample_policy_rows, token_values)
 
 __all__ = [
     "CONFIGS",
@@ -24,4 +24,5 @@ __all__ = [
     "old_logp_from_anchor",
     "perturbed_logps",
     "sample_policy_rows",
+    "token_values",
 ]

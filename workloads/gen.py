@@ -156,6 +156,12 @@ def perturbed_logps(old: np.ndarray, st: Structure, sigma: float, seed: int) -> 
     return np.where(st.mask.astype(bool), out, 0.0).astype(np.float32)
 
 
+def token_values(st: Structure, seed: int, scale: float = 1.0) -> np.ndarray:
+    """Value-model outputs V(s_t) for every packed row: scale * N(0,1) (float32, seeded)."""
+    rng = np.random.Generator(np.random.PCG64(seed))
+    return (float(scale) * rng.standard_normal(st.N)).astype(np.float32)
+
+
 def sample_policy_rows(candidates: np.ndarray, k: int, seed: int) -> np.ndarray:
     """k distinct rows drawn (seeded) from the given candidate positions, sorted."""
     rng = np.random.Generator(np.random.PCG64(seed))
