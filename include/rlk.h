@@ -207,6 +207,49 @@ rlk_status_t rlk_value_loss(int64_t N, int32_t R, const int32_t* cu_seqlens, con
                             const float* values, const float* returns, const int32_t* group_ids, float* loss,
                             float* dvalues, void* ws, size_t ws_bytes, void* stream);
 
+/* Prefix-tree packing of each rollout's model calls (Sec. 3.2.1; the trainable-token rule of
+ * Sec. 3.2.3).  Host code, host pointers; no GPU involved.
+ * Calls of rollout r are call_off[r] .. call_off[r+1]-1, in capture order; call c has the input
+ * context x_tok[x_off[c] .. x_off[c+1]) and the model response y_tok[y_off[c] .. y_off[c+1]).
+ * Tree: rooted at the first call's context (the task prompt); each call attaches to the node
+ * whose accumulated history is the longest prefix of its context (ties: the earliest node) and
+ * adds a node holding the intervening harness tokens (not trainable) followed by its response
+ * (trainable); a node identical to an existing sibling is that sibling.  A context extending no
+ * node's history starts another tree of the rollout.
+ * Packing: per rollout, nodes depth-first (children in first-seen order).  Positions carry the
+ * token, parent (packed index of the previous token on the root path, -1 at a tree's first token)
+ * and depth (index on that path), for the trunk's tree attention and position ids.  Rows, one per
+ * position with a parent: src = parent (the hidden state that predicts the token), target = the
+ * token, mask = 1 for response tokens; row_cu [R+1] segments the rows by rollout and is the
+ * cu_seqlens of the batch the loss entry points take (hidden rows gathered at src).  leaves [R]:
+ * number of leaf nodes (trajectories) per rollout.  All indices are batch-global.
+ * Size query: with every output pointer NULL, fills n_pos and n_rows and returns RLK_OK; with
+ * outputs given, capacities below the need return RLK_ESHAPE (n_pos, n_rows still filled). */
+typedef struct {
+  int32_t R;
+  const int64_t* call_off;  /* [R+1] */
+  const int64_t* x_off;     /* [C+1], C = call_off[R] */
+  const int32_t* x_tok;
+  const int64_t* y_off;     /* [C+1] */
+  const int32_t* y_tok;
+} rlk_calls_t;
+
+typedef struct {
+  int64_t cap_pos, cap_rows;
+  int32_t* token;           /* [cap_pos] */
+  int32_t* parent;          /* [cap_pos] */
+  int32_t* depth;           /* [cap_pos] */
+  int64_t* pos_off;         /* [R+1] */
+  int32_t* row_src;         /* [cap_rows] */
+  int32_t* row_target;      /* [cap_rows] */
+  uint8_t* row_mask;        /* [cap_rows] */
+  int32_t* row_cu;          /* [R+1] */
+  int32_t* leaves;          /* [R] */
+  int64_t n_pos, n_rows;    /* out */
+} rlk_tree_out_t;
+
+rlk_status_t rlk_tree_pack(const rlk_calls_t* calls, rlk_tree_out_t* out);
+
 /* Synchronises `stream`, then reads the status word that the previous calls using `ws`
  * left there.  *flags (optional host pointer) receives RLK_DERR_* bits; returns RLK_OK or
  * RLK_EDATA.  Each entry point clears the word when it starts. */

@@ -19,4 +19,5 @@ from .rl_oracle import (  # noqa: F401
     sampled_rows,
     gae,
     value_loss,
+    tree_pack,
 )

@@ -42,6 +42,9 @@ Readings where the paper is silent (each one is stated where it is applied):
     tokens in order (tool tokens stepped over), the terminal reward arriving at the
     last policy token; a packed rollout is one trajectory; the value loss is the
     token mean of (V - G)^2 over policy tokens, G = A + V;
+  * prefix trees (Sec. 3.2.1): a call attaches to the node whose history is the
+    longest prefix of its context; a node identical to a sibling is that sibling;
+    packing is depth-first, one training row per non-root position;
   * token-level truncated importance sampling (Sec. 3.2.4) is optional (off by
     default); when on, w_t = min(exp(old_t - rollout_t), c_bar) scales the whole
     loss of token t (surrogate, entropy and KL terms) and is held constant in
@@ -424,3 +427,90 @@ def value_loss(values, returns, mask, cu_seqlens, group_ids=None):
     diff = V[idx] - G[idx]
     dV[idx] = 2.0 * diff / idx.size
     return float((diff * diff).mean()), dV
+
+
+# --------------------------------------------------------------------------
+# Prefix-tree packing of a rollout's model calls (Sec. 3.2.1, used by Sec. 3.2.3).
+# --------------------------------------------------------------------------
+def tree_pack(calls_per_rollout):
+    """Prefix trees of the rollouts' model calls, packed for the trainer.
+
+    calls_per_rollout: list over rollouts of lists of (x, y) token lists, in capture order
+    (x = the call's input context, y = the model's response).
+
+    Sec. 3.2.1: the tree is rooted at the initial task prompt, taken to be the first call's
+    context (a harness-content node under an empty root); each call attaches to the existing
+    node whose accumulated history is the longest prefix of x; the new node holds the
+    intervening harness content x[len(history):] (not trainable) followed by y (trainable), and
+    its history is x + y.  A context that extends no node's history (not even the prompt)
+    attaches to the empty root and starts a separate tree of the rollout.
+    Reading: a new node whose content equals that of an existing child of the same parent is
+    that child (identical calls collapse, so a shared history is stored once); children keep
+    their first-seen order.
+
+    Packing, per rollout: the nodes in depth-first pre-order, each node's tokens in order.
+    Every packed position p has parent[p] = the packed position of the previous token on its
+    root path (-1 for the first token of a tree) and depth[p] = its index on that path.
+    Training rows: one per position with parent >= 0, predicting token[p] from the hidden state
+    at parent[p]: row (src = parent[p], target = token[p], mask = 1 if p holds a model-generated
+    token).  Shared prefixes therefore yield each trainable token once per rollout (Sec. 3.2.3),
+    and a fork yields one row per continuation.
+
+    Returns dict(token, parent, depth, pos_off [R+1], row_src, row_target, row_mask,
+    row_cu [R+1], leaves [R]) with positions/rows numbered over the whole batch.
+    """
+    tok, par, dep, pos_off = [], [], [], [0]
+    rsrc, rtgt, rmask, row_cu, leaves = [], [], [], [0], []
+    for calls in calls_per_rollout:
+        # node: dict(hist=list, content=list, mask=list, children=[node ids])
+        nodes = [dict(hist=[], content=[], mask=[], children=[])]
+        if calls and len(calls[0][0]) > 0:
+            prompt = list(calls[0][0])
+            nodes.append(dict(hist=prompt, content=prompt, mask=[0] * len(prompt), children=[]))
+            nodes[0]["children"].append(1)
+        for x, y in calls:
+            x, y = list(x), list(y)
+            best, best_len = 0, -1
+            for k, n in enumerate(nodes):
+                L = len(n["hist"])
+                if L <= len(x) and x[:L] == n["hist"] and L > best_len:
+                    best, best_len = k, L
+            content = x[best_len:] + y
+            mask = [0] * (len(x) - best_len) + [1] * len(y)
+            same = [c for c in nodes[best]["children"]
+                    if nodes[c]["content"] == content and nodes[c]["mask"] == mask]
+            if same or not content:
+                continue
+            nodes.append(dict(hist=x + y, content=content, mask=mask, children=[]))
+            nodes[best]["children"].append(len(nodes) - 1)
+        base = len(tok)
+        nrows = 0
+
+        def emit(k, last_pos, depth):
+            nonlocal nrows
+            n = nodes[k]
+            prev = last_pos
+            for t, m in zip(n["content"], n["mask"]):
+                p = len(tok)
+                tok.append(t)
+                par.append(prev)
+                dep.append(depth)
+                if prev >= 0:
+                    rsrc.append(prev)
+                    rtgt.append(t)
+                    rmask.append(m)
+                    nrows += 1
+                prev = p
+                depth += 1
+            for c in n["children"]:
+                emit(c, prev, depth)
+
+        emit(0, -1, 0)
+        leaves.append(sum(1 for k, n in enumerate(nodes) if k > 0 and not n["children"]))
+        pos_off.append(len(tok))
+        row_cu.append(row_cu[-1] + nrows)
+        assert pos_off[-1] - base >= 0
+    i32 = lambda a: np.asarray(a, dtype=np.int32)
+    return dict(token=i32(tok), parent=i32(par), depth=i32(dep), pos_off=np.asarray(pos_off, np.int64),
+                row_src=i32(rsrc), row_target=i32(rtgt), row_mask=np.asarray(rmask, np.uint8),
+                row_cu=i32(row_cu), leaves=i32(leaves))

@@ -23,7 +23,7 @@ EXPORTS = [
     "rlk_workspace_size", "rlk_advantage_workspace_size", "rlk_compact", "rlk_logprob_fwd", "rlk_group_advantage",
     "rlk_pg_loss_fwd_bwd", "rlk_check_status", "rlk_status_string", "rlk_last_error", "rlk_version",
     "rlk_profile_begin", "rlk_profile_end", "rlk_kernel_kind_name", "rlk_gae", "rlk_value_workspace_size",
-    "rlk_value_loss",
+    "rlk_value_loss", "rlk_tree_pack",
 ]
 
 
@@ -45,6 +45,19 @@ class PgStats(ctypes.Structure):
                 ("clip_frac", ctypes.c_float), ("ratio_mean", ctypes.c_float), ("n_groups", ctypes.c_int32),
                 ("n_valid_rollouts", ctypes.c_int32), ("n_policy_tokens", ctypes.c_int64),
                 ("kl_mean", ctypes.c_float), ("tis_mean", ctypes.c_float)]
+
+
+class Calls(ctypes.Structure):
+    _fields_ = [("R", ctypes.c_int32), ("call_off", ctypes.c_void_p), ("x_off", ctypes.c_void_p),
+                ("x_tok", ctypes.c_void_p), ("y_off", ctypes.c_void_p), ("y_tok", ctypes.c_void_p)]
+
+
+class TreeOut(ctypes.Structure):
+    _fields_ = [("cap_pos", ctypes.c_int64), ("cap_rows", ctypes.c_int64), ("token", ctypes.c_void_p),
+                ("parent", ctypes.c_void_p), ("depth", ctypes.c_void_p), ("pos_off", ctypes.c_void_p),
+                ("row_src", ctypes.c_void_p), ("row_target", ctypes.c_void_p), ("row_mask", ctypes.c_void_p),
+                ("row_cu", ctypes.c_void_p), ("leaves", ctypes.c_void_p), ("n_pos", ctypes.c_int64),
+                ("n_rows", ctypes.c_int64)]
 
 
 class RlkError(RuntimeError):
@@ -85,6 +98,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.rlk_gae.argtypes = [i64, i32, vp, vp, vp, vp, vp, f32, f32, vp, vp, vp]
     lib.rlk_value_workspace_size.argtypes = [i32, ctypes.POINTER(sz)]
     lib.rlk_value_loss.argtypes = [i64, i32, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
+    lib.rlk_tree_pack.argtypes = [ctypes.POINTER(Calls), ctypes.POINTER(TreeOut)]
     lib.rlk_kernel_kind_name.restype = ctypes.c_char_p
     for name in EXPORTS:
         if name not in ("rlk_status_string", "rlk_last_error", "rlk_kernel_kind_name", "rlk_version"):
@@ -291,6 +305,57 @@ def value_loss(values, returns, mask, cu_seqlens, group_ids=None, loss=None, dva
     _check(lib.rlk_value_loss(N, R, _ptr(cu_seqlens), _ptr(mask), _ptr(values), _ptr(returns), _ptr(group_ids),
                               _ptr(loss), _ptr(dvalues), _ptr(ws), ws.numel(), _stream_handle(stream)))
     return loss, dvalues
+
+
+def _calls_struct(calls_per_rollout):
+    """Flat host arrays (kept alive in the returned tuple) and the rlk_calls_t describing them."""
+    import numpy as np
+
+    call_off, x_off, y_off, xs, ys = [0], [0], [0], [], []
+    for calls in calls_per_rollout:
+        for x, y in calls:
+            xs.extend(int(t) for t in x)
+            ys.extend(int(t) for t in y)
+            x_off.append(len(xs))
+            y_off.append(len(ys))
+        call_off.append(len(x_off) - 1)
+    arrs = dict(call_off=np.asarray(call_off, np.int64), x_off=np.asarray(x_off, np.int64),
+                y_off=np.asarray(y_off, np.int64), x_tok=np.asarray(xs, np.int32), y_tok=np.asarray(ys, np.int32))
+    c = Calls(R=len(calls_per_rollout), **{k: v.ctypes.data for k, v in arrs.items()})
+    return c, arrs
+
+
+def tree_pack_sizes(calls_per_rollout):
+    """(packed positions, training rows) that tree_pack will produce."""
+    c, keep = _calls_struct(calls_per_rollout)
+    o = TreeOut()
+    _check(load_library().rlk_tree_pack(ctypes.byref(c), ctypes.byref(o)))
+    return o.n_pos, o.n_rows
+
+
+def tree_pack(calls_per_rollout, cap_pos=None, cap_rows=None) -> dict:
+    """Prefix trees of the rollouts' model calls, packed (see rlk_tree_pack).  calls_per_rollout:
+    list over rollouts of lists of (context tokens, response tokens).  Host numpy arrays."""
+    import numpy as np
+
+    n_pos, n_rows = tree_pack_sizes(calls_per_rollout)
+    cap_pos = n_pos if cap_pos is None else cap_pos
+    cap_rows = n_rows if cap_rows is None else cap_rows
+    R = len(calls_per_rollout)
+    out = dict(token=np.zeros(max(cap_pos, 1), np.int32), parent=np.zeros(max(cap_pos, 1), np.int32),
+               depth=np.zeros(max(cap_pos, 1), np.int32), pos_off=np.zeros(R + 1, np.int64),
+               row_src=np.zeros(max(cap_rows, 1), np.int32), row_target=np.zeros(max(cap_rows, 1), np.int32),
+               row_mask=np.zeros(max(cap_rows, 1), np.uint8), row_cu=np.zeros(R + 1, np.int32),
+               leaves=np.zeros(max(R, 1), np.int32))
+    c, keep = _calls_struct(calls_per_rollout)
+    o = TreeOut(cap_pos=cap_pos, cap_rows=cap_rows, **{k: v.ctypes.data for k, v in out.items()})
+    _check(load_library().rlk_tree_pack(ctypes.byref(c), ctypes.byref(o)))
+    for k in ("token", "parent", "depth"):
+        out[k] = out[k][:o.n_pos]
+    for k in ("row_src", "row_target", "row_mask"):
+        out[k] = out[k][:o.n_rows]
+    out["leaves"] = out["leaves"][:R]
+    return out
 
 
 def check_status(ws, stream=None) -> int:

@@ -39,6 +39,12 @@ rlk_status_t hip_fail(hipError_t e, const char* what) {
   return fail(RLK_EHIP, "%s: %s", what, hipGetErrorString(e));
 }
 
+}  // namespace
+
+rlk_status_t report_error(rlk_status_t code, const char* msg) { return fail(code, "%s", msg); }
+
+namespace {
+
 inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 inline int64_t roundup(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
 

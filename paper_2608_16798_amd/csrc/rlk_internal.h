@@ -194,6 +194,9 @@ hipError_t launch_fwd_gemm(int dtype, const GemmArgs& a, bool store_q, hipStream
 hipError_t launch_dh_gemm(int dtype, const GemmArgs& a, hipStream_t s);
 hipError_t launch_dw_gemm(int dtype, const GemmArgs& a, hipStream_t s);
 
+// ---- error reporting for host-side entry points in other files (rlk_api.hip) ----
+rlk_status_t report_error(rlk_status_t code, const char* msg);
+
 // ---- profiling (rlk_api.hip) ----
 void prof_mark(int kind, bool begin, hipStream_t s);
 
