@@ -120,26 +120,45 @@ k_gather(const T* hidden, int d, const int32_t* idx, const WsHeader* hdr, int64_
 
 // ---- merge of the per-vocabulary-tile partials (m, s, u) into lse, logp, H; loss scalars.
 __global__ void __launch_bounds__(256) k_combine(TokenParams p) {
+  // 64 tokens per block; wavefront w merges the vocabulary tiles k = w, w + 4, ... of its lane's
+  // token (loads coalesced over the 64 tokens), then the four partial results meet in LDS.
+  // Two passes: the maximum M of the tile maxima, then with w_k = e^{m_k - M}
+  //   S = sum_k w_k s_k,  T = sum_k w_k (u_k + (m_k - M) s_k),
+  // so that lse = M + ln S and sum_j p_j (z_j - lse) = T / S - ln S.
+  __shared__ float s_m[4][64];
+  __shared__ double s_S[4][64], s_T[4][64];
   int64_t rc = (int64_t)p.hdr->n_eff - p.c0;
   rc = rc < 0 ? 0 : (rc > p.Mc ? p.Mc : rc);
-  const int64_t tl = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (tl >= rc) return;
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  const int64_t tl = (int64_t)blockIdx.x * 64 + lane;
+  if ((int64_t)blockIdx.x * 64 >= rc) return;
+  const bool act = tl < rc;
+  float mx = -INFINITY;
+  if (act)
+    for (int k = wv; k < p.nvt; k += 4) mx = fmaxf(mx, p.pm[(int64_t)k * p.Mc + tl]);
+  s_m[wv][lane] = mx;
+  __syncthreads();
+  const float M = fmaxf(fmaxf(s_m[0][lane], s_m[1][lane]), fmaxf(s_m[2][lane], s_m[3][lane]));
+  double S = 0.0, T = 0.0;
+  if (act)
+    for (int k = wv; k < p.nvt; k += 4) {
+      const int64_t o = (int64_t)k * p.Mc + tl;
+      const float mk = p.pm[o];
+      const double w = (double)__builtin_amdgcn_exp2f((mk - M) * kLog2e);
+      const double sk = (double)p.ps[o];
+      S += w * sk;
+      T += w * ((double)p.pu[o] + (double)(mk - M) * sk);
+    }
+  s_S[wv][lane] = S;
+  s_T[wv][lane] = T;
+  __syncthreads();
+  if (wv != 0 || !act) return;
+  S = s_S[0][lane] + s_S[1][lane] + s_S[2][lane] + s_S[3][lane];
+  T = s_T[0][lane] + s_T[1][lane] + s_T[2][lane] + s_T[3][lane];
   const int64_t i = p.c0 + tl;
-  float M = -INFINITY;
-  for (int k = 0; k < p.nvt; ++k) M = fmaxf(M, p.pm[(int64_t)k * p.Mc + tl]);
-  double S = 0.0;
-  for (int k = 0; k < p.nvt; ++k) {
-    const int64_t o = (int64_t)k * p.Mc + tl;
-    S += (double)p.ps[o] * (double)__builtin_amdgcn_exp2f((p.pm[o] - M) * kLog2e);
-  }
-  const double lse = (double)M + log(S);
-  // sum_j p_j (z_j - lse) = sum_k e^{m_k - lse} (u_k + (m_k - lse) s_k)
-  double E = 0.0;
-  for (int k = 0; k < p.nvt; ++k) {
-    const int64_t o = (int64_t)k * p.Mc + tl;
-    const double dm = (double)p.pm[o] - lse;
-    E += exp(dm) * ((double)p.pu[o] + dm * (double)p.ps[o]);
-  }
+  const double lnS = log(S);
+  const double lse = (double)M + lnS;
+  const double E = T / S - lnS;
   const float lsef = (float)lse;
   const float H = (float)(-E);
   const float logp = (float)((double)p.zy[i] - lse);
@@ -427,7 +446,7 @@ hipError_t launch_gather(int dtype, const void* hidden, int d, const int32_t* id
 
 hipError_t launch_combine(const TokenParams& p, hipStream_t s) {
   prof_mark(KK_COMBINE, true, s);
-  k_combine<<<(unsigned)((p.Mc + 255) / 256), 256, 0, s>>>(p);
+  k_combine<<<(unsigned)((p.Mc + 63) / 64), 256, 0, s>>>(p);
   prof_mark(KK_COMBINE, false, s);
   return hipGetLastError();
 }
