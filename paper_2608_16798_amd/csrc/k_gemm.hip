@@ -53,9 +53,9 @@ constexpr int OPND_B = kTile * KS;      // one operand's slice
 constexpr int STAGE_B = 2 * OPND_B;     // A + B
 constexpr int PIPE_B = NSTAGE * STAGE_B;
 static_assert(PIPE_B <= 131072 && (KS == 64 || KS == 128) && IPW >= 1, "pipeline geometry");
-constexpr int RED_OFF = 0;              // epilogue reduction scratch (reuses the pipeline buffers)
-constexpr int LDS_B = PIPE_B;
-static_assert(RED_OFF + 3 * WAVES_M * kTile * 4 <= LDS_B, "epilogue scratch");
+constexpr int QROW = kTile * 2 + 16;    // LDS row stride of the bf16 probability tile (bytes)
+constexpr int RED_OFF = kTile * QROW;   // 135168: reduction scratch after the staged tile
+constexpr int LDS_B = RED_OFF + 3 * WAVES_M * kTile * 4;  // >= PIPE_B
 constexpr int GROUP_M = 16;
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr int kBufferFlags = 0x00020000;  // raw buffer: 32-bit data format, offset range-checked
@@ -392,22 +392,18 @@ __global__ void __launch_bounds__(NT) k_gemm(GemmArgs a) {
     }
     __syncthreads();
 
-    // phase 2: e = exp(z - m), s = sum e, u = sum e (z - m); e optionally stored as q (bf16).
-    // Lanes l and l + 32 hold rows 8g + 0..3 and 8g + 4..7 of one column; one swap between the
-    // lane halves (v_permlane32_swap) per register gives lane l all 8 rows of group 2h and lane
-    // l + 32 those of group 2h + 1, stored as two adjacent 16-byte pieces of the column's q row.
+    // phase 2: e = exp(z - m), s = sum e, u = sum e (z - m); e optionally staged for storage.
+    char* sQ = smem;
 #pragma unroll
     for (int nb = 0; nb < NBW; ++nb) {
       const int cl = wn * WTN + nb * 32 + lrow;
-      const int n = tile_n * kTile + cl;
       float mt = red_m[cl];
 #pragma unroll
       for (int w = 1; w < WAVES_M; ++w) mt = fmaxf(mt, red_m[w * kTile + cl]);
       const float mt2 = mt * kLog2e;
       float s = 0.0f, u = 0.0f;
 #pragma unroll
-      for (int mb = 0; mb < MBW; ++mb) {
-        u32x2 pk[4];
+      for (int mb = 0; mb < MBW; ++mb)
 #pragma unroll
         for (int g = 0; g < 4; ++g) {
           float ev[4];
@@ -423,34 +419,22 @@ __global__ void __launch_bounds__(NT) k_gemm(GemmArgs a) {
             ev[i] = e;
           }
           if constexpr (STORE_Q) {
+            const int rl0 = wm * WTM + mb * 32 + g * 8 + lh * 4;
             if constexpr (sizeof(T) == 2) {
-              pk[g].x = pack_bf16x2(ev[0], ev[1]);
-              pk[g].y = pack_bf16x2(ev[2], ev[3]);
-            } else if (n < N) {
-              const int rl0 = wm * WTM + mb * 32 + g * 8 + lh * 4;
-              float* qp = reinterpret_cast<float*>(a.q) + (int64_t)n * a.ldq + v0 + rl0;
+              u32x2 pk;
+              pk.x = pack_bf16x2(ev[0], ev[1]);
+              pk.y = pack_bf16x2(ev[2], ev[3]);
+              *reinterpret_cast<u32x2*>(sQ + cl * QROW + rl0 * 2) = pk;
+            } else {
+              const int n = tile_n * kTile + cl;
+              if (n < N) {
+                float* qp = reinterpret_cast<float*>(a.q) + (int64_t)n * a.ldq + v0 + rl0;
 #pragma unroll
-              for (int i = 0; i < 4; ++i) qp[i] = ev[i];
+                for (int i = 0; i < 4; ++i) qp[i] = ev[i];
+              }
             }
           }
         }
-        if constexpr (STORE_Q && sizeof(T) == 2) {
-#pragma unroll
-          for (int h = 0; h < 2; ++h) {
-            const u32x2 lo = __builtin_amdgcn_permlane32_swap(pk[2 * h].x, pk[2 * h + 1].x, false, false);
-            const u32x2 hi = __builtin_amdgcn_permlane32_swap(pk[2 * h].y, pk[2 * h + 1].y, false, false);
-            if (n < N) {
-              const int rl0 = wm * WTM + mb * 32 + (2 * h + lh) * 8;
-              u32x4 v;
-              v.x = lo.x;
-              v.y = hi.x;
-              v.z = lo.y;
-              v.w = hi.y;
-              *reinterpret_cast<u32x4*>(reinterpret_cast<char*>(a.q) + ((int64_t)n * a.ldq + v0 + rl0) * 2) = v;
-            }
-          }
-        }
-      }
       s += __shfl_xor(s, 32, 64);
       u += __shfl_xor(u, 32, 64);
       if (lh == 0) {
@@ -476,6 +460,20 @@ __global__ void __launch_bounds__(NT) k_gemm(GemmArgs a) {
           a.pm[o] = m;
           a.ps[o] = s;
           a.pu[o] = u;
+        }
+      }
+    }
+    if constexpr (STORE_Q && sizeof(T) == 2) {
+      // phase 3: coalesced copy of the staged bf16 tile to q[n][v0 .. v0 + 255].
+      const int chunk = tid & 31;
+#pragma unroll 4
+      for (int it = 0; it < kTile * 32 / NT; ++it) {
+        const int cl = (tid >> 5) + (NT / 32) * it;
+        const int n = tile_n * kTile + cl;
+        if (n < N) {
+          const u32x4 v = *reinterpret_cast<const u32x4*>(sQ + cl * QROW + chunk * 16);
+          char* dst = reinterpret_cast<char*>(a.q) + ((int64_t)n * a.ldq + v0) * 2 + chunk * 16;
+          *reinterpret_cast<u32x4*>(dst) = v;
         }
       }
     }
