@@ -314,3 +314,30 @@ def test_full_size_sampled_rows(name):
     assert e_lp <= tol and e_en <= tol and e_dh <= TOL_GRAD
     assert rel_cs <= 1e-2
     assert np.isfinite(gpu["loss"])
+
+
+# Ragged shapes: hidden sizes that are not a multiple of the 64-element K slice (the forward GEMM's
+# K tail, the dhidden/dW GEMMs' ragged N), vocabularies that are not a multiple of the 256-row
+# tile (and smaller than one tile), token counts that leave partial token tiles.
+RAGGED = [("tiny_fp32", dict(d=264, V=1000)), ("tiny_fp32", dict(d=40, V=100)),
+          ("small_bf16", dict(d=136, V=777)), ("small_bf16", dict(d=520, V=4099))]
+
+
+@pytest.mark.parametrize("name,kw", RAGGED)
+def test_pg_loss_parity_ragged_shapes(name, kw):
+    base = WL.get_config(name) if name == "tiny_fp32" else WL.scaled_config(name)
+    cfg = base.with_(name=f"{base.name}_d{kw['d']}_V{kw['V']}", w_std=1.0 / np.sqrt(kw["d"]), **kw)
+    inst = build_instance(cfg)
+    p = params_for(cfg, entropy_coef=0.02, chunk_rows=256)
+    log(f"pg_loss ragged {cfg.name} N={inst['st'].N}")
+    compare_full(inst, run_gpu(inst, p), run_oracle(inst, p), p, tag="ragged")
+    # the log-prob forward alone on the same shapes
+    import torch
+
+    ws = rlk.alloc_workspace(rlk.workspace_size(rlk.make_batch(inst["h"], inst["W"], inst["cu"])), "cuda")
+    logp = torch.empty(inst["st"].N, dtype=torch.float32, device="cuda")
+    rlk.logprob_fwd(inst["h"], inst["W"], inst["targets"], inst["mask"], inst["cu"], logp=logp, ws=ws)
+    torch.cuda.synchronize()
+    ref = run_oracle(inst, p, grads=False)
+    err = float(np.abs(logp.cpu().numpy()[ref["idx"]] - ref["logp"]).max())
+    assert err <= TOL_LOGP[cfg.dtype], err
