@@ -5,12 +5,13 @@
 //   dhidden : A = dz [tokens, Vp],   B = W^T [d, Vp]                   -> scatter to dh[idx]
 //   dW      : A = dz^T [Vp, tokens], B = hidden^T [d, tokens]          -> fp32 dW (+)=
 //
-// Tile geometry (gfx950): a 256 x 256 output tile per workgroup of WAVES_M x WAVES_N wavefronts,
-// each owning a (256 / WAVES_M) x (256 / WAVES_N) block of 32 x 32 v_mfma_f32_32x32x16_bf16
-// tiles (fp32 operands use v_mfma_f32_32x32x2_f32), accumulators in AGPRs.  Operands stream
-// through LDS in K slices of KS bytes per row, copied straight from global memory by
-// buffer_load ... lds (no staging registers) into NSTAGE buffers; rows are XOR-swizzled at 16-byte
-// granularity so MFMA fragment reads are bank-conflict free.  Each lane's MFMA fragment carries 8
+// Tile geometry (gfx950): a 256 x 256 output tile per workgroup of WAVES_M x WAVES_N = 2 x 4
+// wavefronts (two per SIMD), each owning a 128 x 64 block of 32 x 32 v_mfma_f32_32x32x16_bf16
+// tiles (fp32 operands use v_mfma_f32_32x32x2_f32) with its 128 fp32 accumulators per lane in
+// the unified register file.  Operands stream through LDS in K slices of KS bytes per row,
+// copied straight from global memory by buffer_load ... lds (no staging registers) into NSTAGE
+// buffers; rows are XOR-swizzled at 16-byte granularity so MFMA fragment reads are bank-conflict
+// free.  Each lane's MFMA fragment carries 8
 // consecutive K elements of one row (16 bytes); A and B use the same K assignment, so the lane
 // split of K inside the MFMA is irrelevant to the sum.
 //
