@@ -278,7 +278,7 @@ def test_device_data_errors_are_flagged():
 
 
 # ------------------------------------------------------------------ full-size, sampled rows
-@pytest.mark.parametrize("name", ["small_bf16", "qwen8b_bf16"])
+@pytest.mark.parametrize("name", ["small_bf16", "qwen8b_bf16", "long_bf16", "large_bf16"])
 def test_full_size_sampled_rows(name):
     """Full-size batch in the configuration the benchmark times: integer outputs bit-exact,
     per-token log-prob / entropy / lse and dhidden rows on seeded sampled rows, dW by the
