@@ -17,6 +17,9 @@ from .rl_oracle import (  # noqa: F401
     kl_sampled,
     pg_loss_fwd_bwd,
     sampled_rows,
+    loss_from_token_values,
+    token_grad_weights,
+    dw_rows,
     gae,
     value_loss,
     tree_pack,

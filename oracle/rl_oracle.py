@@ -379,6 +379,54 @@ def sampled_rows(h_rows, W, y_rows, old_rows, adv_rows, omega_rows, *, eps_low, 
     return out
 
 
+def loss_from_token_values(logp, H, old_logp, adv_tok, tok_rollout, n_pol, gi, G, n_groups, *, eps_low, eps_high,
+                           entropy_coef=0.0, agg=AGG_SEQ, norm_override=None):
+    """Loss -J (Sec. 2.3.1 / 2.3.2 objectives, readings above) of the compacted policy tokens
+    from their log-probs and entropies, for batches too large for a full-logit pass: the
+    aggregation of pg_loss_fwd_bwd applied to given per-token values."""
+    s, _, _ = surrogate(logp, old_logp, adv_tok, eps_low, eps_high)
+    val = s + entropy_coef * _f64(H)
+    R = np.asarray(n_pol).shape[0]
+    return -_aggregate(val, np.asarray(tok_rollout, dtype=np.int64), np.asarray(n_pol), np.asarray(gi),
+                       np.asarray(G), n_groups, R, agg, norm_override)
+
+
+def token_grad_weights(logp, old_logp, adv_tok, omega, *, eps_low, eps_high, entropy_coef=0.0):
+    """Chain-rule weights of the clipped surrogate with the entropy bonus (no importance weight,
+    no KL term): g_t = dL/dlogp_t = omega_t A_t rho_t [not clipped], e_t = dL/dH_t = omega_t c_ent,
+    omega_t from token_weights."""
+    _, rho, clipped = surrogate(logp, old_logp, adv_tok, eps_low, eps_high)
+    om = _f64(omega)
+    return om * _f64(adv_tok) * rho * (~clipped), om * entropy_coef
+
+
+def dw_rows(h, W, v_sel, y, logp, H, g, e, block: int = 8192):
+    """Rows v_sel of dW = sum_t dz_t h_t^T over the compacted policy tokens t, from per-token
+    scalars: the log-prob logp_t, entropy H_t and the chain-rule weights g_t = dL/dlogp_t,
+    e_t = dL/dH_t.  With z_tv = W_v . h_t, lse_t = z_{t,y_t} - logp_t and p_tv = e^{z_tv - lse_t},
+    dz_tv = g_t ([v = y_t] - p_tv) - e_t p_tv (z_tv - lse_t + H_t) (the derivatives noted in
+    pg_loss_fwd_bwd).  h is [n, d], read in row blocks (anything whose slices convert to arrays),
+    W is [V, d]; a row's cost is 2 n d per selected v."""
+    v_sel = np.asarray(v_sel, dtype=np.int64)
+    y = np.asarray(y, dtype=np.int64)
+    logp, H, g, e = _f64(logp), _f64(H), _f64(g), _f64(e)
+    Wsel = _f64(np.asarray(W)[v_sel])
+    n = y.shape[0]
+    out = np.zeros((v_sel.shape[0], Wsel.shape[1]))
+    for b0 in range(0, n, block):
+        b1 = min(n, b0 + block)
+        hb = _f64(h[b0:b1])
+        yb = y[b0:b1]
+        zy = np.einsum("ij,ij->i", hb, _f64(np.asarray(W)[yb]))
+        lse = zy - logp[b0:b1]
+        z = hb @ Wsel.T
+        p = np.exp(z - lse[:, None])
+        dz = -p * (g[b0:b1, None] + e[b0:b1, None] * (z - lse[:, None] + H[b0:b1, None]))
+        dz += g[b0:b1, None] * (yb[:, None] == v_sel[None, :])
+        out += dz.T @ hb
+    return out
+
+
 # --------------------------------------------------------------------------
 # PPO path (Sec. 2.3.1 GAE and value loss; Sec. 3.2.3 simplified variant).
 # --------------------------------------------------------------------------

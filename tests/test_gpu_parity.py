@@ -9,7 +9,7 @@ that the oracle computes one by one and on properties that hold at any size.
 import numpy as np
 import pytest
 
-from gpu_common import (TOL_GRAD, aux_logps, TOL_LOGP, O, WL, build_instance, compare_full, ensure_library, log,
+from gpu_common import (TOL_GRAD, TOL_LOSS, aux_logps, TOL_LOGP, O, WL, build_instance, compare_full, ensure_library, log,
                         params_for, rel_fro, rlk, run_gpu, run_oracle, to_host)
 
 pytestmark = pytest.mark.gpu
@@ -278,11 +278,33 @@ def test_device_data_errors_are_flagged():
 
 
 # ------------------------------------------------------------------ full-size, sampled rows
+class _CompactRows:
+    """Compacted policy rows of a device tensor, fetched to the host block by block."""
+
+    def __init__(self, h, idx):
+        import torch
+
+        self.h = h
+        self.idx = torch.as_tensor(idx, device=h.device)
+        self.shape = (int(idx.shape[0]), int(h.shape[1]))
+
+    def __getitem__(self, sl):
+        return to_host(self.h[self.idx[sl]])
+
+
+N_SAMPLED_ROWS = 1024
+N_DW_ROWS = 64
+
+
 @pytest.mark.parametrize("name", ["small_bf16", "qwen8b_bf16", "long_bf16", "large_bf16"])
 def test_full_size_sampled_rows(name):
-    """Full-size batch in the configuration the benchmark times: integer outputs bit-exact,
-    per-token log-prob / entropy / lse and dhidden rows on seeded sampled rows, dW by the
-    zero column-sum property."""
+    """Full-size batch in the configuration the benchmark times: integer outputs bit-exact;
+    per-token log-prob / entropy and dhidden rows exact on 1,024 seeded sampled rows (a row
+    depends only on itself and per-rollout scalars); the loss re-aggregated in fp64 from the
+    GPU's per-token log-probs and entropies; 64 seeded dW rows from the GPU's per-token values
+    (each is a sum over every policy token); the zero column sum of dW."""
+    import time
+
     import torch
 
     cfg = WL.get_config(name)
@@ -296,24 +318,55 @@ def test_full_size_sampled_rows(name):
     ga = O.group_advantage(st.rewards, st.group_ids, p.adv_eps)
     assert gpu["stats"]["n_policy_tokens"] == idx.shape[0] and gpu["stats"]["n_groups"] == ga["n_groups"]
     omega = O.token_weights(tr, npol, ga["group_index"], ga["G"], ga["n_groups"], p.agg)
-    pick = np.sort(WL.sample_policy_rows(np.arange(idx.shape[0]), 192, seed=cfg.seed + 7))
+    adv_tok = ga["adv"][tr]
+    old_pol = inst["old_host"][idx]
+    W_host = to_host(inst["W"])
+    t0 = time.time()
+
+    # sampled rows: forward and dhidden
+    pick = np.sort(WL.sample_policy_rows(np.arange(idx.shape[0]), N_SAMPLED_ROWS, seed=cfg.seed + 7))
     rows = idx[pick]
     rows_t = torch.as_tensor(rows, device="cuda")
-    ref = O.sampled_rows(to_host(inst["h"][rows_t]), to_host(inst["W"]), st.targets[rows], inst["old_host"][rows],
-                         ga["adv"][tr[pick]], omega[pick], eps_low=p.eps_low, eps_high=p.eps_high,
-                         entropy_coef=p.entropy_coef)
+    ref = O.sampled_rows(to_host(inst["h"][rows_t]), W_host, st.targets[rows], old_pol[pick], adv_tok[pick],
+                         omega[pick], eps_low=p.eps_low, eps_high=p.eps_high, entropy_coef=p.entropy_coef)
     lp = gpu["logp"][rows_t].cpu().numpy()
     en = gpu["ent"][rows_t].cpu().numpy()
     dh = to_host(gpu["dh"][rows_t])
     e_lp, e_en = np.abs(lp - ref["logp"]).max(), np.abs(en - ref["H"]).max()
     e_dh = rel_fro(dh, ref["dh"])
+
+    # loss: the oracle's aggregation of the GPU's per-token values (all policy tokens)
+    idx_t = torch.as_tensor(idx, device="cuda")
+    lp_all = gpu["logp"][idx_t].double().cpu().numpy()
+    en_all = gpu["ent"][idx_t].double().cpu().numpy()
+    loss_ref = O.loss_from_token_values(lp_all, en_all, old_pol, adv_tok, tr, npol, ga["group_index"], ga["G"],
+                                        ga["n_groups"], eps_low=p.eps_low, eps_high=p.eps_high,
+                                        entropy_coef=p.entropy_coef, agg=p.agg)
+    s_tok, _, _ = O.surrogate(lp_all, old_pol, adv_tok, p.eps_low, p.eps_high)
+    scale = float(np.abs(omega * (s_tok + p.entropy_coef * en_all)).sum())
+    e_loss = abs(gpu["loss"] - loss_ref) / max(scale, 1e-30)
+
+    # dW rows: seeded vocabulary ids, a quarter of them targets of policy tokens (the one-hot term)
+    rng = np.random.default_rng(cfg.seed + 11)
+    tgt = st.targets[idx]
+    v_sel = np.unique(np.concatenate([rng.choice(cfg.V, N_DW_ROWS * 3 // 4, replace=False),
+                                      rng.choice(tgt, N_DW_ROWS // 4, replace=False)]))
+    g, e = O.token_grad_weights(lp_all, old_pol, adv_tok, omega, eps_low=p.eps_low, eps_high=p.eps_high,
+                                entropy_coef=p.entropy_coef)
+    dw_ref = O.dw_rows(_CompactRows(inst["h"], idx), W_host, v_sel, tgt, lp_all, en_all, g, e)
+    dw_gpu = gpu["dW"][torch.as_tensor(v_sel, device="cuda")].double().cpu().numpy()
+    e_dw = rel_fro(dw_gpu, dw_ref)
+
     colsum = to_host(gpu["dW"].sum(dim=0))
     rel_cs = float(np.abs(colsum).max() / max(1e-30, float(gpu["dW"].abs().sum(dim=0).max())))
-    log(f"  sampled: logp {e_lp:.3g} ent {e_en:.3g} dh {e_dh:.3g}; dW colsum rel {rel_cs:.3g}")
+    log(f"  {N_SAMPLED_ROWS} sampled rows: logp {e_lp:.3g} ent {e_en:.3g} dh {e_dh:.3g}; loss {e_loss:.3g} "
+        f"(gpu {gpu['loss']:.6g} ref {loss_ref:.6g}); {v_sel.shape[0]} dW rows {e_dw:.3g}; dW colsum rel "
+        f"{rel_cs:.3g}; oracle {time.time() - t0:.1f} s")
     tol = TOL_LOGP[cfg.dtype]
     assert e_lp <= tol and e_en <= tol and e_dh <= TOL_GRAD
+    assert e_loss <= TOL_LOSS
+    assert e_dw <= TOL_GRAD
     assert rel_cs <= 1e-2
-    assert np.isfinite(gpu["loss"])
 
 
 # Ragged shapes: hidden sizes that are not a multiple of the 64-element K slice (the forward GEMM's

@@ -613,3 +613,38 @@ def test_token_advantage_gradients_match_finite_differences():
             bp[name][ij] -= 2e-6
             lm_ = _loss(bp, grads=False, **kw)["loss"]
             assert abs((lp_ - lm_) / 2e-6 - grad[ij]) <= 1e-6 * max(1.0, abs(grad).max())
+
+
+# ------------------------------------- row-restricted helpers used by the full-size GPU checks
+@pytest.mark.parametrize("agg", [O.AGG_SEQ, O.AGG_TOKEN])
+def test_loss_from_token_values_matches_the_full_pass(agg):
+    b = _with_old_from_current(61, excluded=(2,))
+    kw = dict(eps_low=0.2, eps_high=0.28, entropy_coef=0.03, agg=agg)
+    out = _loss(b, **kw)
+    idx, tr, npol = out["idx"], out["tok_rollout"], out["n_pol"]
+    ga = O.group_advantage(b["rewards"], b["group_ids"], EPS)
+    got = O.loss_from_token_values(out["logp"], out["H"], b["old_logp"][idx], ga["adv"][tr], tr, npol,
+                                   ga["group_index"], ga["G"], ga["n_groups"], eps_low=0.2, eps_high=0.28,
+                                   entropy_coef=0.03, agg=agg)
+    np.testing.assert_allclose(got, out["loss"], rtol=1e-12, atol=1e-15)
+    omega = O.token_weights(tr, npol, ga["group_index"], ga["G"], ga["n_groups"], agg)
+    g, e = O.token_grad_weights(out["logp"], b["old_logp"][idx], ga["adv"][tr], omega, eps_low=0.2,
+                                eps_high=0.28, entropy_coef=0.03)
+    np.testing.assert_allclose(g, out["g"], rtol=1e-13, atol=1e-16)
+    np.testing.assert_allclose(e, out["e"], rtol=1e-13, atol=1e-16)
+
+
+def test_dw_rows_match_the_full_gradient():
+    b = _with_old_from_current(62, V=24, excluded=(1,))
+    kw = dict(eps_low=0.2, eps_high=0.28, entropy_coef=0.05)
+    out = _loss(b, **kw)
+    idx = out["idx"]
+    y = b["targets"][idx]
+    # every row, so the selection includes each target id and the zero column sum applies
+    v_all = np.arange(b["W"].shape[0])
+    rows = O.dw_rows(b["h"][idx], b["W"], v_all, y, out["logp"], out["H"], out["g"], out["e"], block=7)
+    np.testing.assert_allclose(rows, out["dW"], rtol=1e-11, atol=1e-14)
+    np.testing.assert_allclose(rows.sum(axis=0), 0.0, atol=1e-13)
+    sel = np.array([y[0], 3, 17, y[-1]])
+    part = O.dw_rows(b["h"][idx], b["W"], sel, y, out["logp"], out["H"], out["g"], out["e"])
+    np.testing.assert_allclose(part, out["dW"][sel], rtol=1e-11, atol=1e-14)
