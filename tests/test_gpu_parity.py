@@ -394,3 +394,31 @@ def test_pg_loss_parity_ragged_shapes(name, kw):
     ref = run_oracle(inst, p, grads=False)
     err = float(np.abs(logp.cpu().numpy()[ref["idx"]] - ref["logp"]).max())
     assert err <= TOL_LOGP[cfg.dtype], err
+
+
+# Degenerate vocabulary: with V = 1 every policy token has log-prob 0, entropy 0 and a zero
+# logit gradient, so dhidden and dW are 0 (one valid row in a 256-row tile); the GPU reaches
+# them up to the fp32 rounding of exp2 / log at z = max.
+@pytest.mark.parametrize("name,d", [("tiny_fp32", 64), ("small_bf16", 128)])
+def test_pg_loss_single_entry_vocabulary(name, d):
+    base = WL.get_config(name) if name == "tiny_fp32" else WL.scaled_config(name)
+    cfg = base.with_(name=f"{base.name}_V1", d=d, V=1, w_std=1.0 / np.sqrt(d))
+    inst = build_instance(cfg)
+    p = params_for(cfg, entropy_coef=0.02)
+    gpu = run_gpu(inst, p)
+    compare_full(inst, gpu, run_oracle(inst, p), p, tag="V=1")
+    assert float(gpu["logp"].abs().max()) <= 1e-6 and float(gpu["ent"].abs().max()) <= 1e-6
+    assert float(gpu["dh"].float().abs().max()) <= 1e-6 and float(gpu["dW"].abs().max()) <= 1e-6
+
+
+# The largest batch the library accepts in rollouts: 16,384 rollouts (2,048 groups of 8) of 8
+# tokens each, many of them with no policy token at all.
+def test_pg_loss_maximum_rollout_count():
+    base = WL.get_config("tiny_fp32")
+    cfg = base.with_(name="tiny_fp32_R16384", groups=2048, rollouts_per_group=8, len_min=8, len_max=8, d=64,
+                     V=512, w_std=1.0 / 8.0, tool_mean=2.0)
+    inst = build_instance(cfg)
+    assert inst["st"].group_ids.shape[0] == 16384   # the documented maximum R
+    p = params_for(cfg, entropy_coef=0.01)
+    log(f"pg_loss max rollouts R={cfg.R} N={inst['st'].N}")
+    compare_full(inst, run_gpu(inst, p), run_oracle(inst, p), p, tag="max R")
