@@ -75,11 +75,16 @@ enum {
   RLK_DERR_CU_SEQLENS = 2  /* cu[0] != 0, cu decreasing, or cu[R] != N */
 };
 
+/* Size limits: the GEMMs address 256-row operand panels with 32-bit buffer offsets, so a
+ * panel (256 rows of d, V or chunk_rows elements) must stay below 2 GiB. */
+#define RLK_MAX_DIM 2097152
+#define RLK_MAX_CHUNK_ROWS 1048576
+
 typedef struct {
   int64_t N;                  /* packed tokens (rows of hidden) */
   int32_t R;                  /* rollouts */
-  int32_t d;                  /* hidden size, multiple of 8 */
-  int32_t V;                  /* vocabulary size */
+  int32_t d;                  /* hidden size, multiple of 8, at most RLK_MAX_DIM */
+  int32_t V;                  /* vocabulary size, 1 .. RLK_MAX_DIM */
   int32_t dtype;              /* RLK_DTYPE_F32 or RLK_DTYPE_BF16 */
   const int32_t* cu_seqlens;  /* device [R+1] */
 } rlk_batch_t;
@@ -93,7 +98,8 @@ typedef struct {
   int32_t accumulate_dW;/* 0: dW is overwritten; 1: the gradient is added to dW */
   double norm_override; /* > 0: replaces Q (SEQ) or the policy-token count (TOKEN) so that
                            micro-batched calls add up to the one-call gradient */
-  int64_t chunk_rows;   /* policy tokens per backward chunk, multiple of 256; 0 = auto */
+  int64_t chunk_rows;   /* policy tokens per backward chunk, multiple of 256, at most
+                           RLK_MAX_CHUNK_ROWS; 0 = auto */
   /* Token-level truncated importance sampling (Sec. 3.2.4): with rollout_logp (device [N] f32,
    * the inference engine's log-prob of each sampled token) the loss of token t is scaled by
    * w_t = min(exp(old_logp[t] - rollout_logp[t]), tis_cap), held constant in the gradient.

@@ -58,12 +58,11 @@ struct Alloc {
 };
 
 bool debug_sync() {
-  static int v = -1;
-  if (v < 0) {
+  static const bool v = [] {
     const char* e = getenv("RLK_DEBUG_SYNC");
-    v = (e && e[0] && e[0] != '0') ? 1 : 0;
-  }
-  return v == 1;
+    return e && e[0] && e[0] != '0';
+  }();
+  return v;
 }
 
 rlk_status_t check_batch(const rlk_batch_t* b) {
@@ -74,7 +73,8 @@ rlk_status_t check_batch(const rlk_batch_t* b) {
   if (b->R == 0 && b->N != 0) return fail(RLK_ESHAPE, "R = 0 with N = %lld tokens", (long long)b->N);
   if (b->R > kMaxRollouts) return fail(RLK_ESHAPE, "R = %d exceeds the supported %d rollouts", b->R, kMaxRollouts);
   if (b->d < 8 || b->d % 8 != 0) return fail(RLK_ESHAPE, "d = %d must be a positive multiple of 8", b->d);
-  if (b->V < 1) return fail(RLK_ESHAPE, "V = %d must be positive", b->V);
+  if (b->d > RLK_MAX_DIM) return fail(RLK_ESHAPE, "d = %d exceeds %d", b->d, RLK_MAX_DIM);
+  if (b->V < 1 || b->V > RLK_MAX_DIM) return fail(RLK_ESHAPE, "V = %d must lie in [1, %d]", b->V, RLK_MAX_DIM);
   if (b->R > 0 && !b->cu_seqlens) return fail(RLK_EINVAL, "cu_seqlens is NULL");
   return RLK_OK;
 }
@@ -86,9 +86,9 @@ rlk_status_t layout(const rlk_batch_t* b, bool bwd, int64_t chunk_rows, WsLayout
   L.nvt = (int32_t)(L.Vp / kVocabTile);
   L.nblk = (int32_t)((N + kScanTile - 1) / kScanTile);
   if (L.nblk < 1) L.nblk = 1;
-  if (chunk_rows < 0 || chunk_rows % kChunkAlign != 0)
-    return fail(RLK_ESHAPE, "chunk_rows = %lld must be a non-negative multiple of %d", (long long)chunk_rows,
-                kChunkAlign);
+  if (chunk_rows < 0 || chunk_rows % kChunkAlign != 0 || chunk_rows > RLK_MAX_CHUNK_ROWS)
+    return fail(RLK_ESHAPE, "chunk_rows = %lld must be a multiple of %d in [0, %d]", (long long)chunk_rows,
+                kChunkAlign, RLK_MAX_CHUNK_ROWS);
   int64_t Mc = chunk_rows;
   if (Mc == 0) {
     int64_t per_row = (int64_t)L.nvt * 12 + d * esz;

@@ -78,6 +78,16 @@ def test_host_validation(lib):
     assert lib.rlk_workspace_size(ctypes.byref(bad), None, ctypes.byref(n)) == rlk.RLK_ESHAPE
     p = rlk.make_params(chunk_rows=300)
     assert lib.rlk_workspace_size(ctypes.byref(b), ctypes.byref(p), ctypes.byref(n)) == rlk.RLK_ESHAPE
+    # size limits of the 32-bit panel addressing
+    p = rlk.make_params(chunk_rows=(1 << 20) + 256)
+    assert lib.rlk_workspace_size(ctypes.byref(b), ctypes.byref(p), ctypes.byref(n)) == rlk.RLK_ESHAPE
+    for field, val in (("V", (1 << 21) + 1), ("d", (1 << 21) + 8), ("V", 0)):
+        bad = _batch(cfg)
+        setattr(bad, field, val)
+        assert lib.rlk_workspace_size(ctypes.byref(bad), None, ctypes.byref(n)) == rlk.RLK_ESHAPE, (field, val)
+    big = _batch(cfg)
+    big.V = 1 << 21
+    assert lib.rlk_workspace_size(ctypes.byref(big), None, ctypes.byref(n)) == rlk.RLK_OK
     assert lib.rlk_advantage_workspace_size(20000, ctypes.byref(n)) == rlk.RLK_ESHAPE
 
     fake = 0x10000  # never dereferenced: every call below fails validation first
