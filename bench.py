@@ -207,6 +207,8 @@ def main():
     ap.add_argument("--steps", type=int, default=5)
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--workload", default="qwen8b_bf16")
+    ap.add_argument("--group-share", type=int, default=1,
+                    help="keep 1/K of the workload's groups: one GPU's share of a K-GPU data-parallel step")
     ap.add_argument("--chunk-rows", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-tokens", type=int, default=1024)
@@ -253,6 +255,10 @@ def main():
     torch.cuda.set_device(0)
 
     cfg = WL.get_config(args.workload)
+    if args.group_share > 1:
+        if cfg.groups % args.group_share:
+            raise SystemExit(f"{cfg.name} has {cfg.groups} groups, not divisible by {args.group_share}")
+        cfg = cfg.with_(name=f"{cfg.name}/{args.group_share}", groups=cfg.groups // args.group_share)
     log(f"[bench] building {cfg.name} inputs")
     inp = build_inputs(cfg)
     st = inp["st"]
