@@ -47,7 +47,7 @@
 extern "C" {
 #endif
 
-#define RLK_VERSION 2
+#define RLK_VERSION 3
 
 typedef int32_t rlk_status_t;
 enum {
@@ -212,6 +212,26 @@ rlk_status_t rlk_value_workspace_size(int32_t R, size_t* bytes);
 rlk_status_t rlk_value_loss(int64_t N, int32_t R, const int32_t* cu_seqlens, const uint8_t* mask,
                             const float* values, const float* returns, const int32_t* group_ids, float* loss,
                             float* dvalues, void* ws, size_t ws_bytes, void* stream);
+
+/* Linear value head for the PPO critic (Sec. 2.3.1: GAE needs V(s_t); the paper leaves the
+ * critic's form open, and with a critic sharing the policy's trunk it is a linear head on the
+ * final hidden state): values[t] = w_v . hidden[t] + b_v on the policy rows (mask = 1, or every
+ * row when mask is NULL) of non-excluded rollouts, 0 on the other rows.  hidden [N, d] and w_v [d]
+ * in the batch dtype (V is not read), values device f32 [N].  Reductions in a fixed order.
+ * Uses no workspace. */
+rlk_status_t rlk_value_head_fwd(const rlk_batch_t* b, const void* hidden, const void* w_v, float b_v,
+                                const uint8_t* mask, const int32_t* group_ids, float* values, void* stream);
+
+/* Its backward for dvalues [N] f32 (e.g. from rlk_value_loss): on the rows rlk_value_head_fwd
+ * computes, dhidden[t] = dvalues[t] w_v, added to dhidden when accumulate = 1 (other rows then
+ * untouched) and written otherwise (other rows then set to 0); dhidden may be NULL (skipped).
+ * dw_v [d] f32 = sum_t dvalues[t] hidden[t] and db_v [1] f32 = sum_t dvalues[t] over those rows,
+ * from per-1024-row partial sums added in row order (deterministic).  ws:
+ * rlk_value_head_workspace_size bytes, 256-byte aligned. */
+rlk_status_t rlk_value_head_workspace_size(const rlk_batch_t* b, size_t* bytes);
+rlk_status_t rlk_value_head_bwd(const rlk_batch_t* b, const void* hidden, const void* w_v, const uint8_t* mask,
+                                const int32_t* group_ids, const float* dvalues, void* dhidden, int32_t accumulate,
+                                float* dw_v, float* db_v, void* ws, size_t ws_bytes, void* stream);
 
 /* Prefix-tree packing of each rollout's model calls (Sec. 3.2.1; the trainable-token rule of
  * Sec. 3.2.3).  Host code, host pointers; no GPU involved.

@@ -22,5 +22,7 @@ from .rl_oracle import (  # noqa: F401
     dw_rows,
     gae,
     value_loss,
+    value_head,
+    value_head_grads,
     tree_pack,
 )

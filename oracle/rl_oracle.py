@@ -41,7 +41,8 @@ Readings where the paper is silent (each one is stated where it is applied):
   * PPO (Sec. 2.3.1, simplified per Sec. 3.2.3): GAE runs over a rollout's policy
     tokens in order (tool tokens stepped over), the terminal reward arriving at the
     last policy token; a packed rollout is one trajectory; the value loss is the
-    token mean of (V - G)^2 over policy tokens, G = A + V;
+    token mean of (V - G)^2 over policy tokens, G = A + V; when the critic shares the
+    policy's trunk, V_t = w_v . h_t + b_v is a linear head on its final hidden state;
   * prefix trees (Sec. 3.2.1): a call attaches to the node whose history is the
     longest prefix of its context; a node identical to a sibling is that sibling;
     packing is depth-first, one training row per non-root position;
@@ -475,6 +476,31 @@ def value_loss(values, returns, mask, cu_seqlens, group_ids=None):
     diff = V[idx] - G[idx]
     dV[idx] = 2.0 * diff / idx.size
     return float((diff * diff).mean()), dV
+
+
+def value_head(h, w_v, b_v, mask, cu_seqlens, group_ids=None):
+    """Value estimates V(s_t) of the PPO objective (Sec. 2.3.1) from a linear value head on the
+    policy's final hidden states (the critic's form is unstated; reading: V_t = w_v . h_t + b_v),
+    on the policy tokens of non-excluded rollouts, 0 elsewhere."""
+    idx, _, _ = compact(mask, cu_seqlens, group_ids)
+    V = np.zeros(np.asarray(h).shape[0])
+    if idx.size:
+        V[idx] = _f64(np.asarray(h)[idx]) @ _f64(w_v) + float(b_v)
+    return V
+
+
+def value_head_grads(h, w_v, dvalues, mask, cu_seqlens, group_ids=None):
+    """Gradients of a loss through value_head given dL/dV (e.g. from value_loss): dL/dh_t =
+    dL/dV_t w_v on the rows value_head computes (0 elsewhere), dL/dw_v = sum_t dL/dV_t h_t and
+    dL/db_v = sum_t dL/dV_t over those rows."""
+    h = np.asarray(h)
+    idx, _, _ = compact(mask, cu_seqlens, group_ids)
+    dV = _f64(dvalues)
+    dh = np.zeros((h.shape[0], h.shape[1]))
+    if idx.size == 0:
+        return dh, np.zeros(h.shape[1]), 0.0
+    dh[idx] = dV[idx, None] * _f64(w_v)[None, :]
+    return dh, dV[idx] @ _f64(h[idx]), float(dV[idx].sum())
 
 
 # --------------------------------------------------------------------------

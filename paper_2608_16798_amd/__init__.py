@@ -23,7 +23,7 @@ EXPORTS = [
     "rlk_workspace_size", "rlk_advantage_workspace_size", "rlk_compact", "rlk_logprob_fwd", "rlk_group_advantage",
     "rlk_pg_loss_fwd_bwd", "rlk_check_status", "rlk_status_string", "rlk_last_error", "rlk_version",
     "rlk_profile_begin", "rlk_profile_end", "rlk_kernel_kind_name", "rlk_gae", "rlk_value_workspace_size",
-    "rlk_value_loss", "rlk_tree_pack",
+    "rlk_value_loss", "rlk_tree_pack", "rlk_value_head_fwd", "rlk_value_head_workspace_size", "rlk_value_head_bwd",
 ]
 
 
@@ -99,6 +99,9 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.rlk_value_workspace_size.argtypes = [i32, ctypes.POINTER(sz)]
     lib.rlk_value_loss.argtypes = [i64, i32, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
     lib.rlk_tree_pack.argtypes = [ctypes.POINTER(Calls), ctypes.POINTER(TreeOut)]
+    lib.rlk_value_head_fwd.argtypes = [ctypes.POINTER(Batch), vp, vp, f32, vp, vp, vp, vp]
+    lib.rlk_value_head_workspace_size.argtypes = [ctypes.POINTER(Batch), ctypes.POINTER(sz)]
+    lib.rlk_value_head_bwd.argtypes = [ctypes.POINTER(Batch), vp, vp, vp, vp, vp, vp, i32, vp, vp, vp, sz, vp]
     lib.rlk_kernel_kind_name.restype = ctypes.c_char_p
     for name in EXPORTS:
         if name not in ("rlk_status_string", "rlk_last_error", "rlk_kernel_kind_name", "rlk_version"):
@@ -305,6 +308,51 @@ def value_loss(values, returns, mask, cu_seqlens, group_ids=None, loss=None, dva
     _check(lib.rlk_value_loss(N, R, _ptr(cu_seqlens), _ptr(mask), _ptr(values), _ptr(returns), _ptr(group_ids),
                               _ptr(loss), _ptr(dvalues), _ptr(ws), ws.numel(), _stream_handle(stream)))
     return loss, dvalues
+
+
+def _head_batch(hidden, cu_seqlens) -> Batch:
+    N, d = hidden.shape
+    return Batch(N=N, R=cu_seqlens.shape[0] - 1, d=d, V=1, dtype=_dtype_code(hidden), cu_seqlens=_ptr(cu_seqlens))
+
+
+def value_head_fwd(hidden, w_v, b_v, mask, cu_seqlens, group_ids=None, values=None, stream=None):
+    """Linear value head values[t] = w_v . hidden[t] + b_v on the policy rows (see rlk_value_head_fwd)."""
+    import torch
+
+    lib = load_library()
+    b = _head_batch(hidden, cu_seqlens)
+    if values is None:
+        values = torch.empty(hidden.shape[0], dtype=torch.float32, device=hidden.device)
+    _check(lib.rlk_value_head_fwd(ctypes.byref(b), _ptr(hidden), _ptr(w_v), ctypes.c_float(b_v), _ptr(mask),
+                                  _ptr(group_ids), _ptr(values), _stream_handle(stream)))
+    return values
+
+
+def value_head_workspace_size(hidden, cu_seqlens) -> int:
+    n = ctypes.c_size_t()
+    b = _head_batch(hidden, cu_seqlens)
+    _check(load_library().rlk_value_head_workspace_size(ctypes.byref(b), ctypes.byref(n)))
+    return n.value
+
+
+def value_head_bwd(hidden, w_v, mask, cu_seqlens, group_ids, dvalues, dhidden=None, accumulate=False, dw_v=None,
+                   db_v=None, ws=None, stream=None):
+    """Backward of the linear value head (see rlk_value_head_bwd); returns (dhidden, dw_v, db_v)."""
+    import torch
+
+    lib = load_library()
+    b = _head_batch(hidden, cu_seqlens)
+    dev = hidden.device
+    if dw_v is None:
+        dw_v = torch.empty(hidden.shape[1], dtype=torch.float32, device=dev)
+    if db_v is None:
+        db_v = torch.empty(1, dtype=torch.float32, device=dev)
+    if ws is None:
+        ws = alloc_workspace(value_head_workspace_size(hidden, cu_seqlens), dev)
+    _check(lib.rlk_value_head_bwd(ctypes.byref(b), _ptr(hidden), _ptr(w_v), _ptr(mask), _ptr(group_ids),
+                                  _ptr(dvalues), _ptr(dhidden), 1 if accumulate else 0, _ptr(dw_v), _ptr(db_v),
+                                  _ptr(ws), ws.numel(), _stream_handle(stream)))
+    return dhidden, dw_v, db_v
 
 
 def _calls_struct(calls_per_rollout):

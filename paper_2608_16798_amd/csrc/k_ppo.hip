@@ -174,7 +174,215 @@ k_value_grad(int64_t N, const int32_t* cu, const uint8_t* mask, const float* val
   }
 }
 
+// ---- linear value head V_t = w . h_t + b on the kept rows (mask = 1, rollout not excluded) and
+// its backward.  Reductions run in a fixed order (wavefront trees, block partials in row order),
+// so results are bitwise reproducible.
+__device__ __forceinline__ int rollout_of_row(const int32_t* cu, int R, int64_t t) {
+  int lo = 0, hi = R - 1;  // first r with cu[r+1] > t, clamped to [0, R-1]
+  while (lo < hi) {
+    const int mid = (lo + hi) >> 1;
+    if ((int64_t)cu[mid + 1] > t) hi = mid; else lo = mid + 1;
+  }
+  return lo;
+}
+
+__device__ __forceinline__ bool kept_row(const uint8_t* mask, const int32_t* cu, const int32_t* gid, int R,
+                                         int64_t t) {
+  if (mask && !mask[t]) return false;
+  return !gid || gid[rollout_of_row(cu, R, t)] >= 0;
+}
+
+template <typename T>
+__device__ __forceinline__ void unpack8(const u32x4 v, float (&f)[16 / sizeof(T)]);
+template <>
+__device__ __forceinline__ void unpack8<bf16_t>(const u32x4 v, float (&f)[8]) {
+  const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    f[2 * i] = __uint_as_float(w[i] << 16);
+    f[2 * i + 1] = __uint_as_float(w[i] & 0xffff0000u);
+  }
+}
+template <>
+__device__ __forceinline__ void unpack8<float>(const u32x4 v, float (&f)[4]) {
+  f[0] = __uint_as_float(v.x);
+  f[1] = __uint_as_float(v.y);
+  f[2] = __uint_as_float(v.z);
+  f[3] = __uint_as_float(v.w);
+}
+__device__ __forceinline__ uint32_t bf16_pair(float lo, float hi) {
+  return (uint32_t)__builtin_bit_cast(uint16_t, (__bf16)lo) | ((uint32_t)__builtin_bit_cast(uint16_t, (__bf16)hi) << 16);
+}
+
+constexpr int kHeadRows = 1024;   // rows per workgroup of the dW partial sums
+
+// one wavefront per row
+template <typename T>
+__global__ void __launch_bounds__(256)
+k_value_head_fwd(int64_t N, int d, const T* h, const T* w, float b, const uint8_t* mask, const int32_t* cu,
+                 const int32_t* gid, int R, float* values) {
+  constexpr int EPC = 16 / sizeof(T);
+  const int64_t t = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (t >= N) return;
+  if (!kept_row(mask, cu, gid, R, t)) {
+    if (lane == 0) values[t] = 0.0f;
+    return;
+  }
+  const T* row = h + t * d;
+  float acc = 0.0f;
+  for (int c = lane; c < d / EPC; c += 64) {
+    float x[EPC], y[EPC];
+    unpack8<T>(*reinterpret_cast<const u32x4*>(row + c * EPC), x);
+    unpack8<T>(*reinterpret_cast<const u32x4*>(w + c * EPC), y);
+#pragma unroll
+    for (int e = 0; e < EPC; ++e) acc = fmaf(x[e], y[e], acc);
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) acc += __shfl_xor(acc, o, 64);
+  if (lane == 0) values[t] = acc + b;
+}
+
+// dhidden rows: kept rows get (dh +) dV_t w, the others are zeroed unless accumulating
+template <typename T>
+__global__ void __launch_bounds__(256)
+k_value_head_dh(int64_t N, int d, const T* w, const float* dv, const uint8_t* mask, const int32_t* cu,
+                const int32_t* gid, int R, T* dh, int accumulate) {
+  constexpr int EPC = 16 / sizeof(T);
+  const int64_t t = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (t >= N) return;
+  const bool keep = kept_row(mask, cu, gid, R, t);
+  if (!keep && accumulate) return;
+  const float g = keep ? dv[t] : 0.0f;
+  T* row = dh + t * d;
+  for (int c = lane; c < d / EPC; c += 64) {
+    float y[EPC], o[EPC];
+    unpack8<T>(*reinterpret_cast<const u32x4*>(w + c * EPC), y);
+    if (accumulate) {
+      unpack8<T>(*reinterpret_cast<const u32x4*>(row + c * EPC), o);
+    } else {
+#pragma unroll
+      for (int e = 0; e < EPC; ++e) o[e] = 0.0f;
+    }
+#pragma unroll
+    for (int e = 0; e < EPC; ++e) o[e] = fmaf(g, y[e], o[e]);
+    u32x4 v;
+    if constexpr (sizeof(T) == 2) {
+      v = u32x4{bf16_pair(o[0], o[1]), bf16_pair(o[2], o[3]), bf16_pair(o[4], o[5]), bf16_pair(o[6], o[7])};
+    } else {
+      v = u32x4{__float_as_uint(o[0]), __float_as_uint(o[1]), __float_as_uint(o[2]), __float_as_uint(o[3])};
+    }
+    *reinterpret_cast<u32x4*>(row + c * EPC) = v;
+  }
+}
+
+// dW partial sums over kHeadRows rows per workgroup: part[blk][j] = sum_t dV_t h_t[j] (fp32, row
+// order), part_db[blk] = sum_t dV_t (fp64); each thread owns 16-byte column chunks.
+template <typename T>
+__global__ void __launch_bounds__(256)
+k_value_head_dw_partial(int64_t N, int d, const T* h, const float* dv, const uint8_t* mask, const int32_t* cu,
+                        const int32_t* gid, int R, float* part, double* part_db) {
+  constexpr int EPC = 16 / sizeof(T);
+  const int64_t t0 = (int64_t)blockIdx.x * kHeadRows, t1 = min(N, t0 + kHeadRows);
+  const int r0 = R > 0 ? rollout_of_row(cu, R, t0) : 0;
+  for (int cb = 0; cb < d / EPC; cb += 256) {
+    const int c = cb + threadIdx.x;
+    float acc[EPC];
+#pragma unroll
+    for (int e = 0; e < EPC; ++e) acc[e] = 0.0f;
+    double db = 0.0;
+    int r = r0;
+    for (int64_t t = t0; t < t1; ++t) {
+      while (r < R - 1 && (int64_t)cu[r + 1] <= t) ++r;
+      const bool keep = (!mask || mask[t]) && (!gid || gid[r] >= 0);
+      const float g = keep ? dv[t] : 0.0f;
+      if (g == 0.0f) continue;
+      db += (double)g;
+      if (c < d / EPC) {
+        float x[EPC];
+        unpack8<T>(*reinterpret_cast<const u32x4*>(h + t * d + c * EPC), x);
+#pragma unroll
+        for (int e = 0; e < EPC; ++e) acc[e] = fmaf(g, x[e], acc[e]);
+      }
+    }
+    if (c < d / EPC) {
+#pragma unroll
+      for (int e = 0; e < EPC; ++e) part[(int64_t)blockIdx.x * d + c * EPC + e] = acc[e];
+    }
+    if (cb == 0 && threadIdx.x == 0) part_db[blockIdx.x] = db;
+  }
+}
+
+// final sums over the workgroup partials, in workgroup order (fp64)
+__global__ void __launch_bounds__(256)
+k_value_head_dw_final(int nblk, int d, const float* part, const double* part_db, float* dw, float* dbias) {
+  const int j = blockIdx.x * 256 + threadIdx.x;
+  if (j < d) {
+    double s = 0.0;
+    for (int b = 0; b < nblk; ++b) s += (double)part[(int64_t)b * d + j];
+    dw[j] = (float)s;
+  }
+  if (blockIdx.x == 0 && threadIdx.x == 0) {
+    double s = 0.0;
+    for (int b = 0; b < nblk; ++b) s += part_db[b];
+    dbias[0] = (float)s;
+  }
+}
+
 }  // namespace
+
+size_t value_head_workspace(int64_t N, int d) {
+  const int64_t nblk = (N + kHeadRows - 1) / kHeadRows;
+  return (size_t)(((nblk * d * 4 + 255) / 256) * 256 + ((nblk * 8 + 255) / 256) * 256);
+}
+
+hipError_t launch_value_head_fwd(int dtype, int64_t N, int d, int R, const void* h, const void* w, float b,
+                                 const uint8_t* mask, const int32_t* cu, const int32_t* gid, float* values,
+                                 hipStream_t s) {
+  if (N == 0) return hipSuccess;
+  prof_mark(KK_VALUE_HEAD, true, s);
+  const unsigned grid = (unsigned)((N + 3) / 4);
+  if (dtype == RLK_DTYPE_BF16)
+    k_value_head_fwd<bf16_t><<<grid, 256, 0, s>>>(N, d, (const bf16_t*)h, (const bf16_t*)w, b, mask, cu, gid, R,
+                                                  values);
+  else
+    k_value_head_fwd<float><<<grid, 256, 0, s>>>(N, d, (const float*)h, (const float*)w, b, mask, cu, gid, R,
+                                                 values);
+  prof_mark(KK_VALUE_HEAD, false, s);
+  return hipGetLastError();
+}
+
+hipError_t launch_value_head_bwd(int dtype, int64_t N, int d, int R, const void* h, const void* w,
+                                 const uint8_t* mask, const int32_t* cu, const int32_t* gid, const float* dv,
+                                 void* dh, int accumulate, float* dw, float* dbias, char* ws, hipStream_t s) {
+  prof_mark(KK_VALUE_HEAD, true, s);
+  const int64_t nblk64 = (N + kHeadRows - 1) / kHeadRows;
+  const int nblk = (int)nblk64;
+  float* part = reinterpret_cast<float*>(ws);
+  double* part_db = reinterpret_cast<double*>(ws + ((nblk64 * d * 4 + 255) / 256) * 256);
+  const bool bf = dtype == RLK_DTYPE_BF16;
+  if (dh && N > 0) {
+    const unsigned grid = (unsigned)((N + 3) / 4);
+    if (bf)
+      k_value_head_dh<bf16_t><<<grid, 256, 0, s>>>(N, d, (const bf16_t*)w, dv, mask, cu, gid, R, (bf16_t*)dh,
+                                                   accumulate);
+    else
+      k_value_head_dh<float><<<grid, 256, 0, s>>>(N, d, (const float*)w, dv, mask, cu, gid, R, (float*)dh,
+                                                  accumulate);
+  }
+  if (nblk > 0) {
+    if (bf)
+      k_value_head_dw_partial<bf16_t><<<nblk, 256, 0, s>>>(N, d, (const bf16_t*)h, dv, mask, cu, gid, R, part,
+                                                           part_db);
+    else
+      k_value_head_dw_partial<float><<<nblk, 256, 0, s>>>(N, d, (const float*)h, dv, mask, cu, gid, R, part,
+                                                          part_db);
+  }
+  k_value_head_dw_final<<<(unsigned)((d + 255) / 256), 256, 0, s>>>(nblk, d, part, part_db, dw, dbias);
+  prof_mark(KK_VALUE_HEAD, false, s);
+  return hipGetLastError();
+}
 
 hipError_t launch_gae(int64_t N, int R, const int32_t* cu, const uint8_t* mask, const float* values,
                       const float* rewards, const int32_t* gid, float gamma, float lam, float* adv, float* ret,

@@ -202,7 +202,7 @@ const char* kKindNames[KK_COUNT_KINDS] = {
     "begin",        "compact_count", "compact_scan",  "compact_write", "rollout_offsets", "group_rank",
     "group_stats",  "advantage",     "transpose_w",   "gather",        "fwd_lse_gemm",    "lse_combine",
     "dz",           "dh_gemm",       "dw_gemm",       "loss_rollout",  "loss_final",      "zero_fill",
-    "gae",          "value_loss"};
+    "gae",          "value_loss",    "value_head"};
 
 }  // namespace
 
@@ -610,6 +610,44 @@ rlk_status_t rlk_value_loss(int64_t N, int32_t R, const int32_t* cu_seqlens, con
   double* part = reinterpret_cast<double*>(w + a.take((size_t)R * 16));
   RLK_TRY(launch_value_loss(N, R, cu_seqlens, mask, values, returns, group_ids, part, total, loss, dvalues, s),
           "value_loss");
+  return RLK_OK;
+}
+
+rlk_status_t rlk_value_head_workspace_size(const rlk_batch_t* b, size_t* bytes) {
+  if (!bytes) return fail(RLK_EINVAL, "bytes is NULL");
+  rlk_status_t st = check_batch(b);
+  if (st) return st;
+  *bytes = value_head_workspace(b->N, b->d);
+  return RLK_OK;
+}
+
+rlk_status_t rlk_value_head_fwd(const rlk_batch_t* b, const void* hidden, const void* w_v, float b_v,
+                                const uint8_t* mask, const int32_t* group_ids, float* values, void* stream) {
+  rlk_status_t st = check_batch(b);
+  if (st) return st;
+  if (!isfinite(b_v)) return fail(RLK_EINVAL, "b_v must be finite");
+  if (b->N > 0 && (!hidden || !w_v || !values)) return fail(RLK_EINVAL, "hidden, w_v or values is NULL");
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  RLK_TRY(launch_value_head_fwd(b->dtype, b->N, b->d, b->R, hidden, w_v, b_v, mask, b->cu_seqlens, group_ids,
+                                values, s),
+          "value_head_fwd");
+  return RLK_OK;
+}
+
+rlk_status_t rlk_value_head_bwd(const rlk_batch_t* b, const void* hidden, const void* w_v, const uint8_t* mask,
+                                const int32_t* group_ids, const float* dvalues, void* dhidden, int32_t accumulate,
+                                float* dw_v, float* db_v, void* ws, size_t ws_bytes, void* stream) {
+  rlk_status_t st = check_batch(b);
+  if (st) return st;
+  if (accumulate != 0 && accumulate != 1) return fail(RLK_EINVAL, "accumulate must be 0 or 1");
+  if (!dw_v || !db_v) return fail(RLK_EINVAL, "dw_v or db_v is NULL");
+  if (b->N > 0 && (!hidden || !w_v || !dvalues)) return fail(RLK_EINVAL, "hidden, w_v or dvalues is NULL");
+  st = check_ws(ws, ws_bytes, value_head_workspace(b->N, b->d));
+  if (st) return st;
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  RLK_TRY(launch_value_head_bwd(b->dtype, b->N, b->d, b->R, hidden, w_v, mask, b->cu_seqlens, group_ids, dvalues,
+                                dhidden, accumulate, dw_v, db_v, static_cast<char*>(ws), s),
+          "value_head_bwd");
   return RLK_OK;
 }
 

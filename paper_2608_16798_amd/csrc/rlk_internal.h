@@ -50,6 +50,7 @@ enum KernelKind {
   KK_ZERO_FILL,
   KK_GAE,
   KK_VALUE_LOSS,
+  KK_VALUE_HEAD,
   KK_COUNT_KINDS
 };
 
@@ -165,6 +166,14 @@ hipError_t launch_gae(int64_t N, int R, const int32_t* cu, const uint8_t* mask, 
 hipError_t launch_value_loss(int64_t N, int R, const int32_t* cu, const uint8_t* mask, const float* values,
                              const float* ret, const int32_t* gid, double* part, double* total, float* loss,
                              float* dv, hipStream_t s);
+
+size_t value_head_workspace(int64_t N, int d);
+hipError_t launch_value_head_fwd(int dtype, int64_t N, int d, int R, const void* h, const void* w, float b,
+                                 const uint8_t* mask, const int32_t* cu, const int32_t* gid, float* values,
+                                 hipStream_t s);
+hipError_t launch_value_head_bwd(int dtype, int64_t N, int d, int R, const void* h, const void* w,
+                                 const uint8_t* mask, const int32_t* cu, const int32_t* gid, const float* dv,
+                                 void* dh, int accumulate, float* dw, float* dbias, char* ws, hipStream_t s);
 
 // ---- launchers (k_gemm.hip) ----
 struct GemmArgs {

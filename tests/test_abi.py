@@ -37,7 +37,7 @@ def test_exports_every_declared_symbol(lib):
 
 
 def test_version_and_strings(lib):
-    assert lib.rlk_version() == 2
+    assert lib.rlk_version() == 3
     assert lib.rlk_status_string(rlk.RLK_EWORKSPACE).decode().startswith("workspace")
     assert lib.rlk_kernel_kind_name(10).decode() == "fwd_lse_gemm"
 
@@ -128,6 +128,18 @@ def test_host_validation(lib):
     assert lib.rlk_value_loss(10, 4, fake, fake, fake, fake, None, fake, None, fake, need - 1, None) \
         == rlk.RLK_EWORKSPACE
     assert lib.rlk_value_loss(10, 4, fake, fake, fake, fake, None, None, None, fake, need, None) == rlk.RLK_EINVAL
+    # linear value head
+    hb = _batch(cfg)
+    assert lib.rlk_value_head_fwd(ctypes.byref(hb), fake, fake, ctypes.c_float(float("nan")), None, None, fake,
+                                  None) == rlk.RLK_EINVAL
+    assert lib.rlk_value_head_fwd(ctypes.byref(hb), None, fake, ctypes.c_float(0.0), None, None, fake,
+                                  None) == rlk.RLK_EINVAL
+    need = ctypes.c_size_t()
+    assert lib.rlk_value_head_workspace_size(ctypes.byref(hb), ctypes.byref(need)) == rlk.RLK_OK
+    assert need.value >= (4096 // 1024) * cfg.d * 4
+    args_h = lambda acc, wsb: (ctypes.byref(hb), fake, fake, None, None, fake, None, acc, fake, fake, fake, wsb, None)
+    assert lib.rlk_value_head_bwd(*args_h(2, need.value)) == rlk.RLK_EINVAL
+    assert lib.rlk_value_head_bwd(*args_h(0, need.value - 1)) == rlk.RLK_EWORKSPACE
     p = rlk.make_params()
     p.accumulate_dW = 2
     assert lib.rlk_pg_loss_fwd_bwd(*args(p)) == rlk.RLK_EINVAL

@@ -107,3 +107,64 @@ def test_ppo_loss_parity(name, scaled, agg):
     gpu = run_gpu(inst, p, token_adv=adv_dev)
     ref = run_oracle(inst, p, token_adv=ra)
     compare_full(inst, gpu, ref, p, tag="ppo")
+
+
+# ------------------------------------------------------------------ linear value head
+HEAD_CASES = [("tiny_fp32", False), ("small_bf16", True), ("qwen8b_bf16", True)]
+
+
+@pytest.mark.parametrize("name,scaled", HEAD_CASES)
+def test_value_head_parity(name, scaled):
+    """values = w_v . h + b_v on the policy rows of non-excluded rollouts; the backward from the
+    value loss (dhidden written and accumulated, dw_v, db_v) against the oracle, bitwise repeatable."""
+    import torch
+
+    from gpu_common import rel_fro, to_host
+
+    ensure_library()
+    cfg = WL.scaled_config(name) if scaled else WL.get_config(name)
+    cfg = cfg.with_(n_excluded=1)
+    inst = build_instance(cfg)
+    st = inst["st"]
+    h = inst["h"]
+    rng = np.random.default_rng(cfg.seed + 77)
+    w_host = (rng.standard_normal(cfg.d) / np.sqrt(cfg.d)).astype(np.float32)
+    w = torch.as_tensor(w_host, device="cuda").to(h.dtype)
+    b_v = 0.25
+    vals = rlk.value_head_fwd(h, w, b_v, inst["mask"], inst["cu"], inst["gid"])
+    torch.cuda.synchronize()
+    h_host, w64 = to_host(h), to_host(w)
+    ref = O.value_head(h_host, w64, b_v, st.mask, st.cu_seqlens, st.group_ids)
+    ev = float(np.abs(vals.cpu().numpy() - ref).max()) / max(1.0, float(np.abs(ref).max()))
+    assert np.all(vals.cpu().numpy()[ref == 0] == 0)
+    # backward of the value loss against seeded returns
+    G = rng.standard_normal(st.N).astype(np.float32)
+    _, dV = O.value_loss(ref, G, st.mask, st.cu_seqlens, st.group_ids)
+    dV_dev = torch.as_tensor(dV.astype(np.float32), device="cuda")
+    r_dh, r_dw, r_db = O.value_head_grads(h_host, w64, dV.astype(np.float32), st.mask, st.cu_seqlens, st.group_ids)
+    dh = torch.full_like(h, 7.0)
+    dh, dw, db = rlk.value_head_bwd(h, w, inst["mask"], inst["cu"], inst["gid"], dV_dev, dhidden=dh)
+    torch.cuda.synchronize()
+    e_dh = rel_fro(to_host(dh), r_dh)
+    e_dw = rel_fro(dw.cpu().numpy(), r_dw)
+    e_db = abs(float(db.item()) - r_db) / max(1e-30, float(np.abs(dV).sum()))
+    # accumulate: kept rows get the gradient added, the other rows keep their values
+    # a base of the gradient's own magnitude, so bf16 rounding of the sum stays relative
+    scale = float(np.abs(r_dh).max())
+    base = torch.as_tensor((scale * rng.standard_normal((st.N, cfg.d))).astype(np.float32), device="cuda").to(h.dtype)
+    acc = base.clone()
+    rlk.value_head_bwd(h, w, inst["mask"], inst["cu"], inst["gid"], dV_dev, dhidden=acc, accumulate=True)
+    _, dw2, db2 = rlk.value_head_bwd(h, w, inst["mask"], inst["cu"], inst["gid"], dV_dev)
+    torch.cuda.synchronize()
+    e_acc = rel_fro(to_host(acc), to_host(base) + r_dh)   # the accumulated result against its exact value
+    keep = np.zeros(st.N, dtype=bool)
+    keep[O.compact(st.mask, st.cu_seqlens, st.group_ids)[0]] = True
+    unchanged = bool(torch.equal(acc[torch.as_tensor(~keep, device="cuda")], base[torch.as_tensor(~keep, device="cuda")]))
+    log(f"value head {cfg.name} N={st.N} d={cfg.d}: values {ev:.2e}, dh {e_dh:.2e}, dw {e_dw:.2e}, db {e_db:.2e}, "
+        f"accumulated dh {e_acc:.2e}")
+    tol_v = 1e-5 if cfg.dtype == "f32" else 1e-4
+    tol_h = 1e-6 if cfg.dtype == "f32" else 1e-2
+    assert ev <= tol_v and e_dh <= tol_h and e_dw <= 1e-5 and e_db <= 1e-6
+    assert e_acc <= (1e-6 if cfg.dtype == "f32" else 1e-2) and unchanged
+    assert torch.equal(dw, dw2) and torch.equal(db, db2)
+    assert int(torch.count_nonzero(dh[torch.as_tensor(~keep, device="cuda")])) == 0

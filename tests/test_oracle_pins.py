@@ -648,3 +648,53 @@ def test_dw_rows_match_the_full_gradient():
     sel = np.array([y[0], 3, 17, y[-1]])
     part = O.dw_rows(b["h"][idx], b["W"], sel, y, out["logp"], out["H"], out["g"], out["e"])
     np.testing.assert_allclose(part, out["dW"][sel], rtol=1e-11, atol=1e-14)
+
+
+# ------------------------------------------------------------- linear value head (PPO critic)
+def test_value_head_closed_form_and_exclusion():
+    c = _gae_case(45)
+    N = c["mask"].shape[0]
+    d = 6
+    h = np.zeros((N, d))
+    h[np.arange(N), np.arange(N) % d] = 1.0          # row t is the unit vector e_{t mod d}
+    w = np.arange(1.0, d + 1.0)
+    V = O.value_head(h, w, 0.5, c["mask"], c["cu"])
+    m = c["mask"].astype(bool)
+    np.testing.assert_array_equal(V[m], w[np.arange(N) % d][m] + 0.5)
+    assert np.all(V[~m] == 0)
+    gid = np.zeros(c["cu"].shape[0] - 1, dtype=np.int64)
+    gid[0] = -1                                       # excluded rollout: no values
+    V2 = O.value_head(h, w, 0.5, c["mask"], c["cu"], gid)
+    assert np.all(V2[c["cu"][0]:c["cu"][1]] == 0)
+
+
+def test_value_head_gradients_match_finite_differences():
+    c = _gae_case(46)
+    rng = np.random.default_rng(47)
+    N = c["mask"].shape[0]
+    d = 5
+    h = rng.standard_normal((N, d))
+    w = rng.standard_normal(d)
+    b = 0.3
+    G = rng.standard_normal(N)
+    gid = np.zeros(c["cu"].shape[0] - 1, dtype=np.int64)
+    gid[-1] = -1
+
+    def loss(hh, ww, bb):
+        return O.value_loss(O.value_head(hh, ww, bb, c["mask"], c["cu"], gid), G, c["mask"], c["cu"], gid)[0]
+
+    _, dV = O.value_loss(O.value_head(h, w, b, c["mask"], c["cu"], gid), G, c["mask"], c["cu"], gid)
+    dh, dw, db = O.value_head_grads(h, w, dV, c["mask"], c["cu"], gid)
+    eps = 1e-6
+    for t in range(N):
+        for j in (0, d - 1):
+            hp, hm = h.copy(), h.copy()
+            hp[t, j] += eps
+            hm[t, j] -= eps
+            np.testing.assert_allclose((loss(hp, w, b) - loss(hm, w, b)) / (2 * eps), dh[t, j], atol=1e-8)
+    for j in range(d):
+        wp, wm = w.copy(), w.copy()
+        wp[j] += eps
+        wm[j] -= eps
+        np.testing.assert_allclose((loss(h, wp, b) - loss(h, wm, b)) / (2 * eps), dw[j], rtol=1e-6, atol=1e-9)
+    np.testing.assert_allclose((loss(h, w, b + eps) - loss(h, w, b - eps)) / (2 * eps), db, rtol=1e-6, atol=1e-9)
