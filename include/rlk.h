@@ -47,7 +47,7 @@
 extern "C" {
 #endif
 
-#define RLK_VERSION 3
+#define RLK_VERSION 4
 
 typedef int32_t rlk_status_t;
 enum {
@@ -87,6 +87,9 @@ typedef struct {
   int32_t V;                  /* vocabulary size, 1 .. RLK_MAX_DIM */
   int32_t dtype;              /* RLK_DTYPE_F32 or RLK_DTYPE_BF16 */
   const int32_t* cu_seqlens;  /* device [R+1] */
+  float temperature;          /* sampling temperature tau of the policy: logits z = W h / tau;
+                                 0 means 1 (the default); otherwise finite and > 0 */
+  int32_t reserved;           /* must be 0 */
 } rlk_batch_t;
 
 typedef struct {

@@ -55,7 +55,7 @@ Readings where the paper is silent (each one is stated where it is applied):
   * group_id < 0 marks an excluded rollout: removed from mu, sigma, G_q, Q and
     the loss; group ids are opaque keys, dense index = rank among the sorted
     distinct non-negative ids;
-  * logits z = W h (no bias, temperature 1);
+  * logits z = W h / tau (no bias; tau = 1 unless a sampling temperature is given);
   * norm_override replaces Q (seq) or the policy-token count (token), so
     gradients of separately processed micro-batches add up to the one-call
     gradient;
@@ -141,10 +141,10 @@ def _logits(h_rows, W):
     return _f64(h_rows) @ _f64(W).T
 
 
-def token_logprob(h_rows, W, y, block: int = 256):
+def token_logprob(h_rows, W, y, block: int = 256, temperature: float = 1.0):
     """log pi(y_t | s_t), entropy and log-partition per row, from complete logit rows.
 
-    z = W h_t; lse = max z + log sum exp(z - max z); logp = z_y - lse;
+    z = W h_t / tau; lse = max z + log sum exp(z - max z); logp = z_y - lse;
     H = -sum_j p_j log p_j with log p_j = z_j - lse.
     """
     W64 = _f64(W)
@@ -155,7 +155,7 @@ def token_logprob(h_rows, W, y, block: int = 256):
     H = np.empty(n)
     for b0 in range(0, n, block):
         b1 = min(n, b0 + block)
-        z = _f64(h_rows[b0:b1]) @ W64.T
+        z = (_f64(h_rows[b0:b1]) @ W64.T) / temperature
         m = z.max(axis=1)
         l = m + np.log(np.exp(z - m[:, None]).sum(axis=1))
         lp = z - l[:, None]
@@ -240,14 +240,15 @@ def _aggregate(val, tok_rollout, n_pol, gi, G, n_groups, R, agg, norm_override):
 def pg_loss_fwd_bwd(h, W, targets, mask, cu_seqlens, old_logp, rewards, group_ids, *,
                     eps_low=0.2, eps_high=0.2, adv_eps=1e-6, entropy_coef=0.0, agg=AGG_SEQ,
                     norm_override=None, rollout_logp=None, tis_cap=None, ref_logp=None, kl_coef=0.0,
-                    token_adv=None, grads=True, block: int = 128):
+                    token_adv=None, temperature=1.0, grads=True, block: int = 128):
     """Loss, per-token outputs and gradients w.r.t. hidden states and the LM-head weight.
 
     h [N, d], W [V, d] (any float dtype, evaluated in fp64), targets [N], mask [N]
     (None = all policy), cu_seqlens [R+1], old_logp [N], rewards [R], group_ids [R];
     rollout_logp [N] with tis_cap switches on truncated importance sampling, ref_logp [N]
     with kl_coef > 0 the KL term; token_adv [N] (PPO, Sec. 2.3.1) replaces the group advantage
-    of each token by a per-token advantage.
+    of each token by a per-token advantage; temperature tau divides the logits (z = W h / tau),
+    so the raw-logit gradient is dL/dz / tau.
     """
     h = np.asarray(h)
     W64 = _f64(W)
@@ -281,7 +282,7 @@ def pg_loss_fwd_bwd(h, W, targets, mask, cu_seqlens, old_logp, rewards, group_id
         b1 = min(n, b0 + block)
         rows = idx[b0:b1]
         hb = _f64(h[rows])
-        z = hb @ W64.T
+        z = (hb @ W64.T) / temperature
         m = z.max(axis=1)
         l = m + np.log(np.exp(z - m[:, None]).sum(axis=1))
         lp = z - l[:, None]
@@ -307,6 +308,7 @@ def pg_loss_fwd_bwd(h, W, targets, mask, cu_seqlens, old_logp, rewards, group_id
             onehot[ar, yb] = 1.0
             # d logp_y / dz_j = [j = y] - p_j ;  d H / dz_j = -p_j (log p_j + H)
             dz = gb[:, None] * (onehot - p) - eb[:, None] * p * (lp + H[b0:b1, None])
+            dz /= temperature   # d z / d (W h) = 1 / tau
             dh[rows] = dz @ W64
             dW += dz.T @ hb
 
@@ -334,7 +336,7 @@ def pg_loss_fwd_bwd(h, W, targets, mask, cu_seqlens, old_logp, rewards, group_id
 
 
 def sampled_rows(h_rows, W, y_rows, old_rows, adv_rows, omega_rows, *, eps_low, eps_high,
-                 entropy_coef=0.0, tis_rows=None, ref_rows=None, kl_coef=0.0, block: int = 64):
+                 entropy_coef=0.0, tis_rows=None, ref_rows=None, kl_coef=0.0, temperature=1.0, block: int = 64):
     """Per-row forward and dhidden for selected policy rows of a large batch.
 
     A row's log-prob, entropy and dhidden depend only on that row and on
@@ -350,7 +352,7 @@ def sampled_rows(h_rows, W, y_rows, old_rows, adv_rows, omega_rows, *, eps_low, 
     for b0 in range(0, n, block):
         b1 = min(n, b0 + block)
         hb = _f64(h_rows[b0:b1])
-        z = hb @ W64.T
+        z = (hb @ W64.T) / temperature
         m = z.max(axis=1)
         l = m + np.log(np.exp(z - m[:, None]).sum(axis=1))
         lp = z - l[:, None]
@@ -376,7 +378,7 @@ def sampled_rows(h_rows, W, y_rows, old_rows, adv_rows, omega_rows, *, eps_low, 
         out["clipped"][b0:b1] = cb
         out["g"][b0:b1] = gb
         out["e"][b0:b1] = eb
-        out["dh"][b0:b1] = dz @ W64
+        out["dh"][b0:b1] = (dz / temperature) @ W64
     return out
 
 
@@ -401,12 +403,12 @@ def token_grad_weights(logp, old_logp, adv_tok, omega, *, eps_low, eps_high, ent
     return om * _f64(adv_tok) * rho * (~clipped), om * entropy_coef
 
 
-def dw_rows(h, W, v_sel, y, logp, H, g, e, block: int = 8192):
+def dw_rows(h, W, v_sel, y, logp, H, g, e, block: int = 8192, temperature: float = 1.0):
     """Rows v_sel of dW = sum_t dz_t h_t^T over the compacted policy tokens t, from per-token
     scalars: the log-prob logp_t, entropy H_t and the chain-rule weights g_t = dL/dlogp_t,
-    e_t = dL/dH_t.  With z_tv = W_v . h_t, lse_t = z_{t,y_t} - logp_t and p_tv = e^{z_tv - lse_t},
+    e_t = dL/dH_t.  With z_tv = W_v . h_t / tau, lse_t = z_{t,y_t} - logp_t and p_tv = e^{z_tv - lse_t},
     dz_tv = g_t ([v = y_t] - p_tv) - e_t p_tv (z_tv - lse_t + H_t) (the derivatives noted in
-    pg_loss_fwd_bwd).  h is [n, d], read in row blocks (anything whose slices convert to arrays),
+    pg_loss_fwd_bwd; the raw-logit gradient is dz / tau).  h is [n, d], read in row blocks (anything whose slices convert to arrays),
     W is [V, d]; a row's cost is 2 n d per selected v."""
     v_sel = np.asarray(v_sel, dtype=np.int64)
     y = np.asarray(y, dtype=np.int64)
@@ -418,13 +420,13 @@ def dw_rows(h, W, v_sel, y, logp, H, g, e, block: int = 8192):
         b1 = min(n, b0 + block)
         hb = _f64(h[b0:b1])
         yb = y[b0:b1]
-        zy = np.einsum("ij,ij->i", hb, _f64(np.asarray(W)[yb]))
+        zy = np.einsum("ij,ij->i", hb, _f64(np.asarray(W)[yb])) / temperature
         lse = zy - logp[b0:b1]
-        z = hb @ Wsel.T
+        z = (hb @ Wsel.T) / temperature
         p = np.exp(z - lse[:, None])
         dz = -p * (g[b0:b1, None] + e[b0:b1, None] * (z - lse[:, None] + H[b0:b1, None]))
         dz += g[b0:b1, None] * (yb[:, None] == v_sel[None, :])
-        out += dz.T @ hb
+        out += (dz / temperature).T @ hb
     return out
 
 

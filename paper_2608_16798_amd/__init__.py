@@ -29,7 +29,8 @@ EXPORTS = [
 
 class Batch(ctypes.Structure):
     _fields_ = [("N", ctypes.c_int64), ("R", ctypes.c_int32), ("d", ctypes.c_int32), ("V", ctypes.c_int32),
-                ("dtype", ctypes.c_int32), ("cu_seqlens", ctypes.c_void_p)]
+                ("dtype", ctypes.c_int32), ("cu_seqlens", ctypes.c_void_p), ("temperature", ctypes.c_float),
+                ("reserved", ctypes.c_int32)]
 
 
 class PgParams(ctypes.Structure):
@@ -136,11 +137,11 @@ def _dtype_code(t) -> int:
     raise TypeError(f"unsupported dtype {t.dtype}")
 
 
-def make_batch(hidden, W, cu_seqlens) -> Batch:
+def make_batch(hidden, W, cu_seqlens, temperature: float = 1.0) -> Batch:
     N, d = hidden.shape
     V = W.shape[0]
     R = cu_seqlens.shape[0] - 1
-    return Batch(N=N, R=R, d=d, V=V, dtype=_dtype_code(W), cu_seqlens=_ptr(cu_seqlens))
+    return Batch(N=N, R=R, d=d, V=V, dtype=_dtype_code(W), cu_seqlens=_ptr(cu_seqlens), temperature=temperature)
 
 
 def make_params(eps_low=0.2, eps_high=None, adv_eps=1e-6, entropy_coef=0.0, agg=AGG_SEQ, accumulate_dW=False,
@@ -185,12 +186,13 @@ def alloc_workspace(nbytes: int, device="cuda"):
     return ws
 
 
-def logprob_fwd(hidden, W, targets, mask, cu_seqlens, logp=None, entropy=None, lse=None, ws=None, stream=None):
+def logprob_fwd(hidden, W, targets, mask, cu_seqlens, logp=None, entropy=None, lse=None, ws=None, stream=None,
+                temperature: float = 1.0):
     """Per-token log-prob / entropy / log-partition of the sampled tokens (rows with mask 0 -> 0)."""
     import torch
 
     lib = load_library()
-    b = make_batch(hidden, W, cu_seqlens)
+    b = make_batch(hidden, W, cu_seqlens, temperature)
     N = b.N
     dev = hidden.device
     if logp is None:
@@ -241,7 +243,7 @@ def group_advantage(rewards, group_ids, adv_eps=1e-6, adv=None, group_index=None
 
 def pg_loss_fwd_bwd(hidden, W, targets, mask, cu_seqlens, old_logp, rewards, group_ids, params: PgParams,
                     loss=None, dhidden=None, dW=None, logp_out=None, entropy_out=None, stats=None, ws=None,
-                    stream=None, rollout_logp=None, ref_logp=None, token_adv=None):
+                    stream=None, rollout_logp=None, ref_logp=None, token_adv=None, temperature: float = 1.0):
     """Loss, dL/dhidden and dL/dW of the masked clipped policy-gradient objective.
     rollout_logp / ref_logp ([N] fp32 device tensors or None) feed truncated importance sampling
     (params.tis_cap) and the KL term (params.kl_coef); token_adv ([N] fp32, e.g. from gae())
@@ -254,7 +256,7 @@ def pg_loss_fwd_bwd(hidden, W, targets, mask, cu_seqlens, old_logp, rewards, gro
         params.rollout_logp = _ptr(rollout_logp)
         params.ref_logp = _ptr(ref_logp)
         params.token_adv = _ptr(token_adv)
-    b = make_batch(hidden, W, cu_seqlens)
+    b = make_batch(hidden, W, cu_seqlens, temperature)
     dev = hidden.device
     if loss is None:
         loss = torch.empty(1, dtype=torch.float32, device=dev)

@@ -353,7 +353,13 @@ __global__ void __launch_bounds__(NT) k_gemm(GemmArgs a) {
   // Accumulator (mb, nb, r) of this lane sits at tile row wm*WTM + mb*32 + 8*(r/4) + 4*lh + r%4 and
   // tile column wn*WTN + nb*32 + lrow.
   if constexpr (EPI == EPI_FWD) {
-    // rows = vocabulary v = v0 + rl, columns = chunk-local token n.
+    // rows = vocabulary v = v0 + rl, columns = chunk-local token n.  Logits z = (W h) / tau.
+    if (a.inv_tau != 1.0f) {
+#pragma unroll
+      for (int mb = 0; mb < MBW; ++mb)
+#pragma unroll
+        for (int nb = 0; nb < NBW; ++nb) acc[mb][nb] *= a.inv_tau;
+    }
     const int v0 = tile_m * kTile;
     const int V = a.V;
     const bool full_v = v0 + kTile <= V;

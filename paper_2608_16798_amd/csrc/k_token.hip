@@ -188,8 +188,9 @@ __global__ void __launch_bounds__(256) k_combine(TokenParams p) {
     double dlogp = clipped ? 0.0 : (double)A * (double)rho;
     // KL term: d/dlogp of -beta (e^r - r - 1), r = ref - logp, is beta (e^r - 1)
     if (p.ref_logp) dlogp += (double)p.kl_coef * (double)expm1f(p.ref_logp[row] - logp);
-    p.gt[i] = (float)(w * dlogp);
-    p.et[i] = (float)(w * (double)p.ent_coef);
+    // g, e are taken per raw logit W h: the temperature's 1 / tau enters here, once
+    p.gt[i] = (float)(w * dlogp * (double)p.inv_tau);
+    p.et[i] = (float)(w * (double)p.ent_coef * (double)p.inv_tau);
   }
 }
 

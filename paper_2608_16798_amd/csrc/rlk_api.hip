@@ -16,7 +16,7 @@
 namespace rlk {
 
 // Layouts the Python binding mirrors.
-static_assert(sizeof(rlk_batch_t) == 32, "rlk_batch_t layout");
+static_assert(sizeof(rlk_batch_t) == 40, "rlk_batch_t layout");
 static_assert(sizeof(rlk_pg_params_t) == 72, "rlk_pg_params_t layout");
 static_assert(sizeof(rlk_pg_stats_t) == 48, "rlk_pg_stats_t layout");
 
@@ -76,8 +76,14 @@ rlk_status_t check_batch(const rlk_batch_t* b) {
   if (b->d > RLK_MAX_DIM) return fail(RLK_ESHAPE, "d = %d exceeds %d", b->d, RLK_MAX_DIM);
   if (b->V < 1 || b->V > RLK_MAX_DIM) return fail(RLK_ESHAPE, "V = %d must lie in [1, %d]", b->V, RLK_MAX_DIM);
   if (b->R > 0 && !b->cu_seqlens) return fail(RLK_EINVAL, "cu_seqlens is NULL");
+  if (b->temperature != 0.0f && !(b->temperature > 0.0f && isfinite(b->temperature)))
+    return fail(RLK_EINVAL, "temperature must be 0 (= 1) or finite and > 0");
+  if (b->reserved != 0) return fail(RLK_EINVAL, "reserved must be 0");
   return RLK_OK;
 }
+
+// 1 / tau of the batch's logits (z = W h / tau)
+float inv_temperature(const rlk_batch_t* b) { return b->temperature == 0.0f ? 1.0f : 1.0f / b->temperature; }
 
 rlk_status_t layout(const rlk_batch_t* b, bool bwd, int64_t chunk_rows, WsLayout& L) {
   const int64_t esz = b->dtype == RLK_DTYPE_BF16 ? 2 : 4;
@@ -291,8 +297,10 @@ rlk_status_t rlk_logprob_fwd(const rlk_batch_t* b, const void* hidden, const voi
     g.ps = reinterpret_cast<float*>(w + L.ps);
     g.pu = reinterpret_cast<float*>(w + L.pu);
     g.V = b->V;
+    g.inv_tau = inv_temperature(b);
     RLK_TRY(launch_fwd_gemm(b->dtype, g, false, s), "fwd_gemm");
     TokenParams tp = {};
+    tp.inv_tau = inv_temperature(b);
     tp.hdr = hdr;
     tp.c0 = c0;
     tp.Mc = L.Mc;
@@ -443,9 +451,11 @@ rlk_status_t rlk_pg_loss_fwd_bwd(const rlk_batch_t* b, const void* hidden, const
     g.q = w + L.q;
     g.ldq = L.Vp;
     g.V = b->V;
+    g.inv_tau = inv_temperature(b);
     RLK_TRY(launch_fwd_gemm(b->dtype, g, true, s), "fwd_gemm");
 
     TokenParams tp = {};
+    tp.inv_tau = inv_temperature(b);
     tp.hdr = hdr;
     tp.c0 = c0;
     tp.Mc = L.Mc;

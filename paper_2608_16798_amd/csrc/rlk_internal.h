@@ -122,6 +122,7 @@ struct TokenParams {
   const float* ref_logp;       // KL term (NULL = off)
   float kl_coef;
   const float* token_adv;      // per-token advantages (NULL = group advantages)
+  float inv_tau;               // 1 / temperature: dL/d(W h) = dL/dz / tau
 };
 hipError_t launch_combine(const TokenParams& p, hipStream_t s);
 
@@ -191,6 +192,7 @@ struct GemmArgs {
   void* q;               // [Mc][ldq]
   int64_t ldq;
   int V;
+  float inv_tau;         // logits z = acc / tau
   // dhidden epilogue
   void* out;
   const int32_t* idx;

@@ -84,7 +84,7 @@ def aux_logps(inst, *, rollout_sigma=0.15, ref_sigma=0.3):
                 ref=torch.as_tensor(rf, device=dev))
 
 
-def run_gpu(inst, params, *, gid=None, mask="default", dW=None, ws=None, aux=None, token_adv=None):
+def run_gpu(inst, params, *, gid=None, mask="default", dW=None, ws=None, aux=None, token_adv=None, temperature=1.0):
     import torch
 
     h, W = inst["h"], inst["W"]
@@ -96,14 +96,14 @@ def run_gpu(inst, params, *, gid=None, mask="default", dW=None, ws=None, aux=Non
         h, W, inst["targets"], inst["mask"] if mask == "default" else mask, inst["cu"], inst["old"],
         inst["rewards"], inst["gid"] if gid is None else gid, params, dW=dW, logp_out=logp, entropy_out=ent,
         stats=stats, ws=ws, rollout_logp=aux["rollout"] if aux else None, ref_logp=aux["ref"] if aux else None,
-        token_adv=token_adv)
+        token_adv=token_adv, temperature=temperature)
     torch.cuda.synchronize()
     flags = rlk.check_status(ws)
     return dict(loss=float(loss.item()), dh=dh, dW=dWo, logp=logp, ent=ent, stats=rlk.stats_from_tensor(stats),
                 flags=flags, ws=ws)
 
 
-def run_oracle(inst, params, *, grads=True, aux=None, token_adv=None):
+def run_oracle(inst, params, *, grads=True, aux=None, token_adv=None, temperature=1.0):
     st = inst["st"]
     extra = {} if token_adv is None else dict(token_adv=token_adv)
     if aux is not None and params.tis_cap > 0:
@@ -114,7 +114,8 @@ def run_oracle(inst, params, *, grads=True, aux=None, token_adv=None):
         to_host(inst["h"]), to_host(inst["W"]), st.targets, st.mask, st.cu_seqlens, inst["old_host"],
         st.rewards, st.group_ids, eps_low=params.eps_low, eps_high=params.eps_high, adv_eps=params.adv_eps,
         entropy_coef=params.entropy_coef, agg=params.agg,
-        norm_override=params.norm_override if params.norm_override > 0 else None, grads=grads, **extra)
+        norm_override=params.norm_override if params.norm_override > 0 else None, temperature=temperature,
+        grads=grads, **extra)
 
 
 def rel_fro(a, b):

@@ -37,7 +37,7 @@ def test_exports_every_declared_symbol(lib):
 
 
 def test_version_and_strings(lib):
-    assert lib.rlk_version() == 3
+    assert lib.rlk_version() == 4
     assert lib.rlk_status_string(rlk.RLK_EWORKSPACE).decode().startswith("workspace")
     assert lib.rlk_kernel_kind_name(10).decode() == "fwd_lse_gemm"
 
@@ -116,6 +116,18 @@ def test_host_validation(lib):
         p.ref_logp = rf
         assert lib.rlk_pg_loss_fwd_bwd(*args(p)) == rlk.RLK_EINVAL, (kw, ro, rf)
     assert ctypes.sizeof(rlk.PgParams) == 72 and ctypes.sizeof(rlk.PgStats) == 48
+    assert ctypes.sizeof(rlk.Batch) == 40
+    for tau in (-1.0, float("inf"), float("nan")):
+        bad = _batch(cfg)
+        bad.temperature = tau
+        assert lib.rlk_workspace_size(ctypes.byref(bad), None, ctypes.byref(n)) == rlk.RLK_EINVAL, tau
+    bad = _batch(cfg)
+    bad.reserved = 1
+    assert lib.rlk_workspace_size(ctypes.byref(bad), None, ctypes.byref(n)) == rlk.RLK_EINVAL
+    for tau in (0.0, 0.5, 2.0):
+        ok = _batch(cfg)
+        ok.temperature = tau
+        assert lib.rlk_workspace_size(ctypes.byref(ok), None, ctypes.byref(n)) == rlk.RLK_OK
     # GAE / value loss
     assert lib.rlk_gae(10, 2, fake, fake, fake, fake, None, ctypes.c_float(1.5), ctypes.c_float(1.0), fake, None,
                        None) == rlk.RLK_EINVAL

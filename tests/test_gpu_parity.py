@@ -422,3 +422,23 @@ def test_pg_loss_maximum_rollout_count():
     p = params_for(cfg, entropy_coef=0.01)
     log(f"pg_loss max rollouts R={cfg.R} N={inst['st'].N}")
     compare_full(inst, run_gpu(inst, p), run_oracle(inst, p), p, tag="max R")
+
+
+# Sampling temperature: logits z = W h / tau in the forward and the gradients.
+@pytest.mark.parametrize("name,scaled,tau", [("tiny_fp32", False, 0.7), ("small_bf16", True, 1.3)])
+def test_pg_loss_temperature_parity(name, scaled, tau):
+    import torch
+
+    cfg = WL.scaled_config(name) if scaled else WL.get_config(name)
+    inst = build_instance(cfg)
+    p = params_for(cfg, entropy_coef=0.02, chunk_rows=256 if scaled else 0)
+    log(f"pg_loss temperature {tau} {cfg.name} N={inst['st'].N}")
+    compare_full(inst, run_gpu(inst, p, temperature=tau), run_oracle(inst, p, temperature=tau), p, tag=f"tau={tau}")
+    logp, ent, lse, ws = rlk.logprob_fwd(inst["h"], inst["W"], inst["targets"], inst["mask"], inst["cu"],
+                                         entropy=torch.empty(inst["st"].N, device="cuda"),
+                                         lse=torch.empty(inst["st"].N, device="cuda"), temperature=tau)
+    torch.cuda.synchronize()
+    idx = O.compact(inst["st"].mask, inst["st"].cu_seqlens)[0]
+    rl, rp, rH = O.token_logprob(to_host(inst["h"])[idx], to_host(inst["W"]), inst["st"].targets[idx], temperature=tau)
+    tol = TOL_LOGP[cfg.dtype]
+    assert np.abs(logp.cpu().numpy()[idx] - rp).max() <= tol and np.abs(ent.cpu().numpy()[idx] - rH).max() <= tol

@@ -318,8 +318,8 @@ def test_empty_batch():
 
 
 # ---------------------------------------------------------------- gradients
-def _kink_safe(b, eps_low, eps_high, margin=1e-3):
-    lse, lp, H = O.token_logprob(b["h"], b["W"], b["targets"])
+def _kink_safe(b, eps_low, eps_high, margin=1e-3, temperature=1.0):
+    lse, lp, H = O.token_logprob(b["h"], b["W"], b["targets"], temperature=temperature)
     rho = np.exp(lp - b["old_logp"])
     for bound in (1 - eps_low, 1 + eps_high):
         near = np.abs(rho - bound) < margin
@@ -698,3 +698,48 @@ def test_value_head_gradients_match_finite_differences():
         wm[j] -= eps
         np.testing.assert_allclose((loss(h, wp, b) - loss(h, wm, b)) / (2 * eps), dw[j], rtol=1e-6, atol=1e-9)
     np.testing.assert_allclose((loss(h, w, b + eps) - loss(h, w, b - eps)) / (2 * eps), db, rtol=1e-6, atol=1e-9)
+
+
+# ------------------------------------------------- sampling temperature (logits z = W h / tau)
+def test_temperature_is_a_rescaled_lm_head():
+    # z = W h / tau is the tau = 1 computation with W / tau: the same loss, log-probs and dhidden,
+    # and dW scaled by 1 / tau (chain rule through W -> W / tau)
+    b = _with_old_from_current(81, excluded=(1,))
+    tau = 0.7
+    kw = dict(eps_low=0.2, eps_high=0.28, entropy_coef=0.03)
+    out = _loss(b, temperature=tau, **kw)
+    b1 = dict(b)
+    b1["W"] = b["W"] / tau
+    ref = _loss(b1, **kw)
+    np.testing.assert_allclose(out["loss"], ref["loss"], rtol=1e-12)
+    np.testing.assert_allclose(out["logp"], ref["logp"], rtol=1e-12, atol=1e-14)
+    np.testing.assert_allclose(out["dh"], ref["dh"], rtol=1e-11, atol=1e-15)
+    np.testing.assert_allclose(out["dW"], ref["dW"] / tau, rtol=1e-11, atol=1e-15)
+    lse, lp, H = O.token_logprob(b["h"][out["idx"]], b["W"], b["targets"][out["idx"]], temperature=tau)
+    np.testing.assert_allclose(lp, out["logp"], rtol=1e-12, atol=1e-14)
+
+
+def test_temperature_gradients_match_finite_differences():
+    b = _with_old_from_current(82, excluded=(2,))
+    tau = 1.6
+    b = _kink_safe(b, 0.2, 0.28, temperature=tau)
+    kw = dict(eps_low=0.2, eps_high=0.28, entropy_coef=0.05, temperature=tau)
+    out = _loss(b, **kw)
+    rng = np.random.default_rng(83)
+    step = 1e-6
+    for name, grad in (("h", out["dh"]), ("W", out["dW"])):
+        X = b[name]
+        for _ in range(15):
+            ij = tuple(rng.integers(0, s) for s in X.shape)
+            bp = dict(b)
+            bp[name] = X.copy()
+            bp[name][ij] += step
+            lp_ = _loss(bp, grads=False, **kw)["loss"]
+            bp[name][ij] -= 2 * step
+            lm_ = _loss(bp, grads=False, **kw)["loss"]
+            assert abs((lp_ - lm_) / (2 * step) - grad[ij]) <= 1e-6 * max(1.0, abs(grad).max()), (name, ij)
+    # the row-restricted helpers follow the same temperature
+    idx = out["idx"]
+    rows = O.dw_rows(b["h"][idx], b["W"], np.arange(b["W"].shape[0]), b["targets"][idx], out["logp"], out["H"],
+                     out["g"], out["e"], temperature=tau)
+    np.testing.assert_allclose(rows, out["dW"], rtol=1e-10, atol=1e-14)
