@@ -471,7 +471,9 @@ __global__ void __launch_bounds__(NT) k_gemm(GemmArgs a) {
       }
     }
     if constexpr (STORE_Q && sizeof(T) == 2) {
-      // phase 3: coalesced copy of the staged bf16 tile to q[n][v0 .. v0 + 255].
+      // phase 3: coalesced copy of the staged bf16 tile to q[n][v0 .. v0 + 255].  q is read once,
+      // by the dz kernel after this launch: non-temporal stores keep it from displacing the
+      // operand panels that later tiles of this launch re-read from the caches.
       const int chunk = tid & 31;
 #pragma unroll 4
       for (int it = 0; it < kTile * 32 / NT; ++it) {
@@ -480,7 +482,7 @@ __global__ void __launch_bounds__(NT) k_gemm(GemmArgs a) {
         if (n < N) {
           const u32x4 v = *reinterpret_cast<const u32x4*>(sQ + cl * QROW + chunk * 16);
           char* dst = reinterpret_cast<char*>(a.q) + ((int64_t)n * a.ldq + v0) * 2 + chunk * 16;
-          *reinterpret_cast<u32x4*>(dst) = v;
+          __builtin_nontemporal_store(v, reinterpret_cast<u32x4*>(dst));
         }
       }
     }
