@@ -12,6 +12,10 @@ same run holds a plain device copy of known size, then
   python bench.py --traffic-summary FETCH.csv WRITE.csv [--workload ...]
 writes profiles/<kernel>_<workload>_traffic.txt (HBM bytes per launch, scaled by the copy's
 known/measured ratio, tagged with a digest of the kernel sources).
+
+Shader clock and MFMA pipe occupancy of the GEMMs: one step under rocprofv3 with
+GRBM_GUI_ACTIVE SQ_VALU_MFMA_BUSY_CYCLES SQ_WAVE_CYCLES SQ_WAIT_ANY, then
+  python bench.py --occupancy-summary COUNTERS.csv TITLE COMMAND
 """
 from __future__ import annotations
 
@@ -176,6 +180,43 @@ def traffic_summary(fetch_csv, write_csv, workload, copy_mib, cmd_fetch, cmd_wri
     return paths
 
 
+N_XCD, N_SIMD = 8, 1024   # MI355X: GRBM_GUI_ACTIVE is summed over the XCDs; MFMA busy over the SIMDs
+
+
+def occupancy_summary(counter_csv, title, cmd):
+    """Shader clock and MFMA pipe occupancy of the three GEMMs from one rocprofv3 counter pass
+    (GRBM_GUI_ACTIVE, SQ_VALU_MFMA_BUSY_CYCLES, SQ_WAVE_CYCLES, SQ_WAIT_ANY): clock = active cycles
+    per XCD / dispatch time, occupancy = MFMA-busy cycles per SIMD / active cycles per XCD.  Launches
+    shorter than 1 ms (chunks past the policy tokens) are left out."""
+    import csv
+    import re
+
+    per = {}
+    for r in csv.DictReader(open(counter_csv)):
+        m = re.search(r"k_gemm<[^,]+, (\d)", r["Kernel_Name"])
+        if not m:
+            continue
+        d = per.setdefault(KERNEL_KIND[m.group(1)], {}).setdefault(r["Dispatch_Id"], {})
+        d[r["Counter_Name"]] = d.get(r["Counter_Name"], 0.0) + float(r["Counter_Value"])
+        d["ns"] = int(r["End_Timestamp"]) - int(r["Start_Timestamp"])
+    out = [f"# {title}", f"# command: {cmd}",
+           "# summary: python bench.py --occupancy-summary <counter_collection.csv> (launches >= 1 ms)",
+           f"# clock = GRBM_GUI_ACTIVE / {N_XCD} / time; occupancy = SQ_VALU_MFMA_BUSY_CYCLES / {N_SIMD} / "
+           f"(GRBM_GUI_ACTIVE / {N_XCD}); wait = SQ_WAIT_ANY / SQ_WAVE_CYCLES",
+           f"{'kernel':14s} {'launches':>8s} {'avg_ms':>8s} {'clock_GHz':>9s} {'mfma_occ':>8s} {'wait':>6s}"]
+    for kind in GEMM_KINDS:
+        runs = [d for d in per.get(kind, {}).values() if d["ns"] >= 1_000_000 and "GRBM_GUI_ACTIVE" in d]
+        if not runs:
+            continue
+        ns = sum(d["ns"] for d in runs)
+        cyc = sum(d["GRBM_GUI_ACTIVE"] for d in runs) / N_XCD
+        busy = sum(d["SQ_VALU_MFMA_BUSY_CYCLES"] for d in runs) / N_SIMD
+        wait = sum(d["SQ_WAIT_ANY"] for d in runs) / max(1.0, sum(d["SQ_WAVE_CYCLES"] for d in runs))
+        out.append(f"{kind:14s} {len(runs):8d} {ns / len(runs) / 1e6:8.2f} {cyc / ns:9.2f} {busy / cyc:8.3f} "
+                   f"{wait:6.3f}")
+    return "\n".join(out) + "\n"
+
+
 def stats_summary(stats_csv, title, cmd):
     """Text table of the rlk kernels from a rocprofv3 --stats kernel summary CSV."""
     import csv
@@ -221,7 +262,13 @@ def main():
     ap.add_argument("--pmc-commands", nargs=2, default=("", ""), help=argparse.SUPPRESS)
     ap.add_argument("--stats-summary", nargs=3, metavar=("STATS_CSV", "TITLE", "COMMAND"),
                     help="print a text table of the rlk kernels from a rocprofv3 --stats CSV and exit")
+    ap.add_argument("--occupancy-summary", nargs=3, metavar=("COUNTER_CSV", "TITLE", "COMMAND"),
+                    help="print shader clock and MFMA occupancy of the GEMMs from a rocprofv3 counter CSV and exit")
     args = ap.parse_args()
+
+    if args.occupancy_summary:
+        sys.stdout.write(occupancy_summary(*args.occupancy_summary))
+        return
 
     if args.stats_summary:
         sys.stdout.write(stats_summary(*args.stats_summary))
