@@ -252,6 +252,8 @@ def main():
                     help="keep 1/K of the workload's groups: one GPU's share of a K-GPU data-parallel step")
     ap.add_argument("--chunk-rows", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--graph", action="store_true",
+                    help="capture one step as a HIP graph and replay it (launch-bound workloads); no per-kernel events")
     ap.add_argument("--cpu-tokens", type=int, default=1024)
     ap.add_argument("--no-kernel-events", action="store_true",
                     help="time the steps without per-kernel HIP events (roofline then null)")
@@ -321,12 +323,12 @@ def main():
     dh = torch.empty_like(inp["h"])
     dW = torch.empty(inp["W"].shape, dtype=torch.float32, device=dev)
     stats = rlk.stats_buffer(dev)
-    stream = torch.cuda.current_stream()
 
     def step():
-        rlk.group_advantage(inp["rewards"], inp["gid"], params.adv_eps, adv=adv, ws=ws_adv, stream=stream)
+        # both calls go to torch's current stream (the capture stream while a graph is recorded)
+        rlk.group_advantage(inp["rewards"], inp["gid"], params.adv_eps, adv=adv, ws=ws_adv)
         rlk.pg_loss_fwd_bwd(inp["h"], inp["W"], inp["targets"], inp["mask"], inp["cu"], inp["old"], inp["rewards"],
-                            inp["gid"], params, loss=loss, dhidden=dh, dW=dW, stats=stats, ws=ws, stream=stream)
+                            inp["gid"], params, loss=loss, dhidden=dh, dW=dW, stats=stats, ws=ws)
 
     if args.calibrate_copy_mib > 0:
         n = args.calibrate_copy_mib * (1 << 20) // 4
@@ -345,14 +347,29 @@ def main():
     s = rlk.stats_from_tensor(stats)
     n_eff = int(s["n_policy_tokens"])
 
+    run = step
+    if args.graph:
+        # one step captured as a HIP graph (the library enqueues kernel launches only), replayed per step
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            step()
+        torch.cuda.current_stream().wait_stream(side)
+        torch.cuda.synchronize()
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            step()
+        torch.cuda.synchronize()
+        run = graph.replay
+        log("[bench] step captured as a graph")
     log(f"[bench] timing {args.steps} step(s)")
-    use_events = not args.no_kernel_events
+    use_events = not args.no_kernel_events and not args.graph
     torch.cuda.synchronize()
     if use_events:
         rlk.profile_begin()
     t0 = time.perf_counter()
     for _ in range(args.steps):
-        step()
+        run()
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     kern = rlk.profile_end() if use_events else {}
@@ -391,7 +408,8 @@ def main():
         "metric": METRIC, "value": round(value, 1), "unit": "policy tokens/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": round(ms_per_step, 3), "higher_is_better": True, "scaling": "weak",
         "vs_baseline": None, "dtype": cfg.dtype, "data": "synthetic",
-        "config": dict(WL.configs.describe(cfg, N), N_eff=n_eff, chunk_rows=args.chunk_rows or "auto"),
+        "config": dict(WL.configs.describe(cfg, N), N_eff=n_eff, chunk_rows=args.chunk_rows or "auto",
+                       **({"graph": True} if args.graph else {})),
         "mfma_pct_of_peak": round(100 * mfma_frac, 2),
         "roofline": roofline, "cpu_baseline": cpu, "kernels": per_kernel,
     }
