@@ -15,12 +15,17 @@
 // consecutive K elements of one row (16 bytes); A and B use the same K assignment, so the lane
 // split of K inside the MFMA is irrelevant to the sum.
 //
+// The gradient GEMMs of shapes with few output tiles split K over several workgroups per tile
+// (fp32 partials in the workspace, summed in split order by k_splitk_reduce).
+//
 // Output layout of a 32x32 MFMA block: lane l holds column (l % 32); accumulator register r
 // holds row 8*(r/4) + 4*(l/32) + (r%4).  With vocabulary on M and tokens on N, every lane's
 // accumulators belong to a single token, so the vocabulary reduction of the online
 // log-softmax is in-register, then one cross-half exchange, then one LDS exchange between
 // the wavefronts of a column.
 #include "rlk_internal.h"
+
+#include <algorithm>
 
 namespace rlk {
 
@@ -43,7 +48,7 @@ constexpr int WTM = kTile / WAVES_M;    // rows of a wavefront's block
 constexpr int WTN = kTile / WAVES_N;    // columns of a wavefront's block
 constexpr int MBW = WTM / 32;           // 32x32 MFMA tiles per wavefront along M
 constexpr int NBW = WTN / 32;           // ... along N
-constexpr int KS = RLK_KS;              // bytes of K per pipeline slice per row (64 or 128)
+constexpr int KS = RLK_KS;              // bytes of K per pipeline slice per row (kGemmSliceBytes)
 constexpr int NSTAGE = RLK_NSTAGE;      // LDS buffers in the copy pipeline
 constexpr int CPR = KS / 16;            // 16-byte chunks per row of a slice
 constexpr int RPI = 64 / CPR;           // rows per LDS-DMA instruction
@@ -53,7 +58,7 @@ constexpr int DMA_PER_SLICE = 2 * IPW;  // vector-memory instructions per wavefr
 constexpr int OPND_B = kTile * KS;      // one operand's slice
 constexpr int STAGE_B = 2 * OPND_B;     // A + B
 constexpr int PIPE_B = NSTAGE * STAGE_B;
-static_assert(PIPE_B <= 131072 && (KS == 64 || KS == 128) && IPW >= 1, "pipeline geometry");
+static_assert(PIPE_B <= 131072 && KS == kGemmSliceBytes && IPW >= 1, "pipeline geometry");
 constexpr int QROW = kTile * 2 + 16;    // LDS row stride of the bf16 probability tile (bytes)
 constexpr int RED_OFF = kTile * QROW;   // 135168: reduction scratch after the staged tile
 constexpr int LDS_B = RED_OFF + 3 * WAVES_M * kTile * 4;  // >= PIPE_B
@@ -218,7 +223,13 @@ __global__ void __launch_bounds__(NT) k_gemm(GemmArgs a) {
       (void*)(reinterpret_cast<const char*>(a.B) + (int64_t)tile_n * kTile * ldb_b), (short)0,
       (int)((uint32_t)rows_b * ldb_b), kBufferFlags);
   const int64_t Kb = (int64_t)K * sizeof(T);
-  const int nk = (int)((Kb + KS - 1) / KS);
+  int nk = (int)((Kb + KS - 1) / KS);
+  // split K: this workgroup covers slices [ks0, ks0 + nk) of the tile's K range
+  int ks0 = 0;
+  if (EPI != EPI_FWD && a.ksplit > 1) {
+    ks0 = (int)blockIdx.y * a.kslices;
+    nk = max(0, min(nk, ks0 + a.kslices) - ks0);
+  }
 
   // Direct global->LDS copies (LDS DMA): one instruction moves 64 lanes x 16 bytes into 1 KiB of
   // LDS at consecutive addresses, i.e. RPI rows of one K slice.  Wave w fills rows
@@ -239,7 +250,7 @@ __global__ void __launch_bounds__(NT) k_gemm(GemmArgs a) {
   // copies of slice kt for the rows owned by wavefront w
   auto dma_w = [&](int kt, int w) {
     char* st = smem + (kt % NSTAGE) * STAGE_B;
-    const uint32_t kb = (uint32_t)kt * KS;
+    const uint32_t kb = (uint32_t)(kt + ks0) * KS;
 #pragma unroll
     for (int j = 0; j < IPW; ++j) {
       const uint32_t r0 = (uint32_t)((w * IPW + j) * RPI);
@@ -352,6 +363,26 @@ __global__ void __launch_bounds__(NT) k_gemm(GemmArgs a) {
   // ------------------------------------------------------------------ epilogues
   // Accumulator (mb, nb, r) of this lane sits at tile row wm*WTM + mb*32 + 8*(r/4) + 4*lh + r%4 and
   // tile column wn*WTN + nb*32 + lrow.
+  if constexpr (EPI != EPI_FWD) {
+    if (a.ksplit > 1) {
+      // split K: fp32 partial of this K range; the reduction kernel applies the epilogue
+      float* part = a.part + (int64_t)blockIdx.y * a.mp * a.ldp;
+#pragma unroll
+      for (int mb = 0; mb < MBW; ++mb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int rl = tile_m * kTile + wm * WTM + mb * 32 + (r >> 2) * 8 + lh * 4 + (r & 3);
+          if (rl < M) {
+#pragma unroll
+            for (int nb = 0; nb < NBW; ++nb) {
+              const int cl = tile_n * kTile + wn * WTN + nb * 32 + lrow;
+              if (cl < N) part[(int64_t)rl * a.ldp + cl] = acc[mb][nb][r];
+            }
+          }
+        }
+      return;
+    }
+  }
   if constexpr (EPI == EPI_FWD) {
     // rows = vocabulary v = v0 + rl, columns = chunk-local token n.  Logits z = (W h) / tau.
     if (a.inv_tau != 1.0f) {
@@ -526,7 +557,45 @@ __global__ void __launch_bounds__(NT) k_gemm(GemmArgs a) {
   }
 }
 
+// Split-K reduction: out = sum of the partials in split order (deterministic), then the dhidden
+// scatter or the dW overwrite / accumulate.  Rows and the empty-chunk rule follow the GEMM.
+template <typename T, int EPI>
+__global__ void __launch_bounds__(256) k_splitk_reduce(GemmArgs a) {
+  int64_t rc = (int64_t)a.hdr->n_eff - a.c0;
+  rc = rc < 0 ? 0 : (rc > a.Mc ? a.Mc : rc);
+  int M = a.M;
+  if (EPI == EPI_DH) M = (int)rc;
+  if (EPI == EPI_DW && rc == 0 && a.c0 > 0) return;
+  const int N = a.N;
+  const int64_t total = (int64_t)M * N;
+  const bool add = EPI == EPI_DW && (a.accumulate || a.c0 > 0);
+  for (int64_t e = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; e < total; e += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t m = e / N, n = e - m * N;
+    float acc = 0.0f;
+    for (int y = 0; y < a.ksplit; ++y) acc += a.part[((int64_t)y * a.mp + m) * a.ldp + n];
+    if constexpr (EPI == EPI_DH) {
+      const int64_t row = a.idx[a.c0 + m];
+      store_elem<T>(reinterpret_cast<T*>(a.out) + row * a.ldo + n, acc);
+    } else {
+      float* p = a.dw + m * a.ldo + n;
+      *p = add ? *p + acc : acc;
+    }
+  }
+}
+
 inline unsigned tiles(int64_t n) { return (unsigned)((n + kTile - 1) / kTile); }
+
+template <typename T, int EPI>
+hipError_t grad_impl(const GemmArgs& a, unsigned ntiles, hipStream_t s) {
+  const unsigned ny = a.ksplit > 1 ? (unsigned)a.ksplit : 1u;
+  k_gemm<T, EPI, false, false><<<dim3(ntiles, ny), NT, 0, s>>>(a);
+  if (a.ksplit > 1) {
+    const int64_t total = (int64_t)a.M * a.N;
+    const unsigned blocks = (unsigned)std::min<int64_t>((total + 255) / 256, 8192);
+    k_splitk_reduce<T, EPI><<<blocks, 256, 0, s>>>(a);
+  }
+  return hipGetLastError();
+}
 
 template <typename T>
 hipError_t fwd_impl(const GemmArgs& a, bool store_q, hipStream_t s) {
@@ -552,25 +621,19 @@ hipError_t launch_fwd_gemm(int dtype, const GemmArgs& a, bool store_q, hipStream
 }
 
 hipError_t launch_dh_gemm(int dtype, const GemmArgs& a, hipStream_t s) {
-  dim3 grid(tiles(a.Mc) * tiles(a.N));
+  const unsigned nt = tiles(a.Mc) * tiles(a.N);
   prof_mark(KK_DH_GEMM, true, s);
-  if (dtype == RLK_DTYPE_BF16)
-    k_gemm<bf16_t, EPI_DH, false, false><<<grid, NT, 0, s>>>(a);
-  else
-    k_gemm<float, EPI_DH, false, false><<<grid, NT, 0, s>>>(a);
+  hipError_t e = dtype == RLK_DTYPE_BF16 ? grad_impl<bf16_t, EPI_DH>(a, nt, s) : grad_impl<float, EPI_DH>(a, nt, s);
   prof_mark(KK_DH_GEMM, false, s);
-  return hipGetLastError();
+  return e;
 }
 
 hipError_t launch_dw_gemm(int dtype, const GemmArgs& a, hipStream_t s) {
-  dim3 grid(tiles(a.M) * tiles(a.N));
+  const unsigned nt = tiles(a.M) * tiles(a.N);
   prof_mark(KK_DW_GEMM, true, s);
-  if (dtype == RLK_DTYPE_BF16)
-    k_gemm<bf16_t, EPI_DW, false, false><<<grid, NT, 0, s>>>(a);
-  else
-    k_gemm<float, EPI_DW, false, false><<<grid, NT, 0, s>>>(a);
+  hipError_t e = dtype == RLK_DTYPE_BF16 ? grad_impl<bf16_t, EPI_DW>(a, nt, s) : grad_impl<float, EPI_DW>(a, nt, s);
   prof_mark(KK_DW_GEMM, false, s);
-  return hipGetLastError();
+  return e;
 }
 
 }  // namespace rlk

@@ -7,6 +7,7 @@
 #include <stdlib.h>
 #include <string.h>
 
+#include <algorithm>
 #include <mutex>
 #include <string>
 #include <vector>
@@ -82,6 +83,17 @@ rlk_status_t check_batch(const rlk_batch_t* b) {
   return RLK_OK;
 }
 
+// split-K arguments of a gradient GEMM (rows of the partial buffer padded to whole tiles)
+void set_split(GemmArgs& g, const SplitK& p, char* part) {
+  g.ksplit = p.s;
+  g.kslices = p.kslices;
+  if (p.s > 1) {
+    g.part = reinterpret_cast<float*>(part);
+    g.ldp = (int64_t)(g.N + kTile - 1) / kTile * kTile;
+    g.mp = (int64_t)(g.M + kTile - 1) / kTile * kTile;
+  }
+}
+
 // 1 / tau of the batch's logits (z = W h / tau)
 float inv_temperature(const rlk_batch_t* b) { return b->temperature == 0.0f ? 1.0f : 1.0f / b->temperature; }
 
@@ -143,6 +155,11 @@ rlk_status_t layout(const rlk_batch_t* b, bool bwd, int64_t chunk_rows, WsLayout
     L.q = a.take((size_t)(Mc * L.Vp * esz));
     L.dzt = a.take((size_t)(L.Vp * Mc * esz));
     L.wt = a.take((size_t)(d * L.Vp * esz));
+    // split-K partials of the dhidden and dW GEMMs (used one after the other)
+    L.sk_dh = splitk_plan(Mc, d, L.Vp * esz);
+    L.sk_dw = splitk_plan(V, d, Mc * esz);
+    const size_t pb = std::max(splitk_bytes(Mc, d, L.sk_dh), splitk_bytes(V, d, L.sk_dw));
+    if (pb > 0) L.part = a.take(pb);
   }
   L.total = a.off;
   return RLK_OK;
@@ -524,6 +541,7 @@ rlk_status_t rlk_pg_loss_fwd_bwd(const rlk_batch_t* b, const void* hidden, const
     h.out = dhidden;
     h.idx = I(L.idx);
     h.ldo = b->d;
+    set_split(h, L.sk_dh, w + L.part);
     RLK_TRY(launch_dh_gemm(b->dtype, h, s), "dh_gemm");
 
     GemmArgs k = {};
@@ -540,6 +558,7 @@ rlk_status_t rlk_pg_loss_fwd_bwd(const rlk_batch_t* b, const void* hidden, const
     k.dw = dW;
     k.ldo = b->d;
     k.accumulate = p->accumulate_dW;
+    set_split(k, L.sk_dw, w + L.part);
     RLK_TRY(launch_dw_gemm(b->dtype, k, s), "dw_gemm");
   }
 

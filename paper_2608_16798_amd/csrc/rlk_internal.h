@@ -25,6 +25,35 @@ constexpr int kTile = 256;       // BM = BN = 256
 constexpr int kVocabTile = 256;  // vocabulary rows per forward tile = per online-LSE partial
 constexpr int kChunkAlign = 256; // chunk_rows granularity
 constexpr int kKAlign = 64;      // K padding of the chunk buffers (bf16 elements per stage)
+constexpr int kGemmSliceBytes = 128;  // bytes of K per GEMM pipeline slice and row
+
+// Split-K plan of a gradient GEMM with at most mmax x n outputs and kbytes of K per row: with
+// fewer than 128 output tiles the K range is split over s workgroups per tile (each at least 4
+// slices), so the launch still fills the GPU; the fp32 partials go to a workspace buffer of
+// s x (rows rounded to 256) x (n rounded to 256) and a reduction kernel adds them in split order.
+struct SplitK {
+  int s;        // splits (1 = none)
+  int kslices;  // K slices per split
+};
+inline SplitK splitk_plan(int64_t mmax, int64_t n, int64_t kbytes) {
+  const int64_t tiles = ((mmax + kTile - 1) / kTile) * ((n + kTile - 1) / kTile);
+  const int64_t nk = (kbytes + kGemmSliceBytes - 1) / kGemmSliceBytes;
+  SplitK p = {1, (int)(nk > 0 ? nk : 1)};
+  if (tiles <= 0 || tiles >= 128) return p;
+  int64_t s = 512 / tiles;
+  if (s > nk / 4) s = nk / 4;
+  if (s > 64) s = 64;
+  if (s < 2) return p;
+  const int64_t ks = (nk + s - 1) / s;
+  p.s = (int)((nk + ks - 1) / ks);
+  p.kslices = (int)ks;
+  if (p.s < 2) p = {1, (int)nk};
+  return p;
+}
+inline size_t splitk_bytes(int64_t mmax, int64_t n, const SplitK& p) {
+  if (p.s < 2) return 0;
+  return (size_t)p.s * (size_t)((mmax + kTile - 1) / kTile * kTile) * (size_t)((n + kTile - 1) / kTile * kTile) * 4;
+}
 constexpr int kScanTile = 4096;  // tokens per compaction block
 constexpr int kMaxRollouts = 16384;
 constexpr int kRollSums = 8;     // per-rollout fp64 sums of the loss reduction
@@ -81,6 +110,8 @@ struct WsLayout {
   size_t q = 0;                    // T [Mc][Vp]
   size_t dzt = 0;                  // T [Vp][Mc]
   size_t wt = 0;                   // T [d][Vp]
+  size_t part = 0;                 // float split-K partials of the dhidden / dW GEMMs (0 = none)
+  SplitK sk_dh = {1, 1}, sk_dw = {1, 1};
   int64_t Mc = 0;                  // chunk rows
   int64_t Vp = 0;                  // vocabulary padded to 256
   int32_t nvt = 0;                 // vocabulary tiles
@@ -200,6 +231,14 @@ struct GemmArgs {
   // dW epilogue
   float* dw;
   int accumulate;
+  // split K (dhidden and dW): ksplit workgroups per output tile, each over kslices slices, write
+  // fp32 partials part[split][row][col] (row stride ldp, mp rows per split); a reduction kernel
+  // then applies the epilogue
+  int ksplit;
+  int kslices;
+  float* part;
+  int64_t ldp;
+  int64_t mp;
 };
 hipError_t launch_fwd_gemm(int dtype, const GemmArgs& a, bool store_q, hipStream_t s);
 hipError_t launch_dh_gemm(int dtype, const GemmArgs& a, hipStream_t s);
