@@ -396,6 +396,28 @@ def test_pg_loss_parity_ragged_shapes(name, kw):
     assert err <= TOL_LOGP[cfg.dtype], err
 
 
+# Split K: with d = 256 and V = 4096 the dhidden and dW GEMMs have fewer than 128 output tiles, so
+# both split K and reduce fp32 partials.  Several chunks exercise the dW accumulation across
+# chunks.  accumulate_dW adds the gradient to a preset dW (expected: preset + oracle gradient).
+def test_split_k_accumulates_into_preset_dw():
+    import torch
+
+    cfg = WL.get_config("tiny_fp32")
+    inst = build_instance(cfg)
+    p = params_for(cfg, chunk_rows=256)
+    ref = run_oracle(inst, p)
+    compare_full(inst, run_gpu(inst, p), ref, p, tag="split-k")
+    g = torch.Generator(device="cuda").manual_seed(11)
+    dW0 = torch.randn(inst["W"].shape, generator=g, device="cuda", dtype=torch.float32)
+    pa = params_for(cfg, chunk_rows=256, accumulate_dW=True)
+    out = run_gpu(inst, pa, dW=dW0.clone())
+    expect = to_host(dW0).astype(np.float64) + ref["dW"]
+    err = float(np.abs(to_host(out["dW"]) - expect).max())
+    scale = float(np.abs(ref["dW"]).max())
+    log(f"split-K accumulate: max |dW - (dW0 + ref)| = {err:.3g} (ref max {scale:.3g})")
+    assert err <= 2e-2 * scale + 1e-6
+
+
 # Degenerate vocabulary: with V = 1 every policy token has log-prob 0, entropy 0 and a zero
 # logit gradient, so dhidden and dW are 0 (one valid row in a 256-row tile); the GPU reaches
 # them up to the fp32 rounding of exp2 / log at z = max.
