@@ -223,7 +223,7 @@ def stats_summary(stats_csv, title, cmd):
     import re
 
     def short(n):
-        m = re.search(r"k_gemm<rlk::(\w+), (\d), (\w+), (\w+)>", n)
+        m = re.search(r"k_gemm<(?:rlk::)?(\w+), (\d), (\w+), (\w+)>", n)
         if m:
             kind = ["fwd_lse", "dh", "dw"][int(m.group(2))]
             return f"k_gemm<{m.group(1)},{kind},store_q={m.group(3)},ktail={m.group(4)}>"
