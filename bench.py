@@ -217,6 +217,62 @@ def occupancy_summary(counter_csv, title, cmd):
     return "\n".join(out) + "\n"
 
 
+HBM_KERNELS = ("k_dz", "k_gather", "k_transpose_w", "k_zero_fill", "k_combine")
+
+
+def hbm_kernel_summary(fetch_csv, write_csv, workload, copy_mib, cmd_fetch, cmd_write):
+    """HBM bytes per step of the bandwidth-bound kernels (FETCH_SIZE / WRITE_SIZE scaled by the
+    calibration copy, as for the GEMMs) against their algorithmic bytes per step."""
+    import csv
+    import re
+
+    import numpy as np
+
+    import workloads as WL
+
+    cfg = WL.get_config(workload)
+    st = WL.make_structure(cfg)
+    n_eff = int(np.asarray(st.mask, dtype=np.int64).sum())
+    esz = 2 if cfg.dtype == "bf16" else 4
+    vp = (cfg.V + 255) // 256 * 256
+    alg = {"k_dz": 3 * n_eff * vp * esz, "k_gather": 3 * n_eff * cfg.d * esz,
+           "k_transpose_w": (cfg.V + vp) * cfg.d * esz, "k_zero_fill": (st.N - n_eff) * (cfg.d * esz + 8),
+           "k_combine": n_eff * (12 * (vp // 256) + 40)}
+    what = {"k_dz": "read q, write dz and dz^T", "k_gather": "read h rows, write h_c and h_c^T",
+            "k_transpose_w": "read W, write W^T", "k_zero_fill": "zero untrained rows of dh, logp, entropy",
+            "k_combine": "read the online-LSE partials, write per-token values"}
+
+    def per_kernel(path):
+        tot = {}
+        for r in csv.DictReader(open(path)):
+            m = re.search(r"rlk::\(anonymous namespace\)::(k_\w+)", r["Kernel_Name"])
+            name = m.group(1) if m else ("copy" if COPY_TAG in r["Kernel_Name"] else None)
+            if name in HBM_KERNELS or name == "copy":
+                d = tot.setdefault(name, {})
+                d[r["Dispatch_Id"]] = d.get(r["Dispatch_Id"], 0.0) + float(r["Counter_Value"])
+        return tot
+
+    fetch, write = per_kernel(fetch_csv), per_kernel(write_csv)
+    known_kib = copy_mib * 1024.0
+    kf, kw = known_kib / max(fetch["copy"].values()), known_kib / max(write["copy"].values())
+    path = os.path.join(PROFILES, f"hbm_kernels_{workload}_traffic.txt")
+    with open(path, "w") as f:
+        f.write(f"# HBM traffic of the bandwidth-bound kernels on the {workload} workload, one step, rocprofv3 "
+                f"counters (N_eff = {n_eff})\n")
+        f.write(f"# fetch pass: {cmd_fetch}\n# write pass: {cmd_write}\n")
+        f.write(f"# summary: python bench.py --traffic-summary <fetch csv> <write csv> --workload {workload} "
+                f"--calibrate-copy-mib {copy_mib}\n")
+        f.write(f"# scales from the calibration copy: fetch {kf:.4f}, write {kw:.4f}\n")
+        f.write(f"{'kernel':15s} {'launches':>8s} {'hbm_GB':>9s} {'alg_GB':>9s} {'ratio':>6s}  algorithmic bytes\n")
+        for k in HBM_KERNELS:
+            if k not in fetch or k not in write:
+                continue
+            hbm = (sum(fetch[k].values()) * kf + sum(write[k].values()) * kw) * 1024.0
+            f.write(f"{k:15s} {len(fetch[k]):8d} {hbm / 1e9:9.3f} {alg[k] / 1e9:9.3f} {hbm / alg[k]:6.3f}  "
+                    f"{what[k]}\n")
+    return path
+
+
 def stats_summary(stats_csv, title, cmd):
     """Text table of the rlk kernels from a rocprofv3 --stats kernel summary CSV."""
     import csv
@@ -281,6 +337,7 @@ def main():
             raise SystemExit("--traffic-summary needs the --calibrate-copy-mib size the runs used")
         for p in traffic_summary(*args.traffic_summary, args.workload, args.calibrate_copy_mib, *args.pmc_commands):
             print(p)
+        print(hbm_kernel_summary(*args.traffic_summary, args.workload, args.calibrate_copy_mib, *args.pmc_commands))
         return
 
     if args.gpus != 1:

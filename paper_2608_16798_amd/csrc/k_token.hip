@@ -121,10 +121,11 @@ k_gather(const T* hidden, int d, const int32_t* idx, const WsHeader* hdr, int64_
 // ---- merge of the per-vocabulary-tile partials (m, s, u) into lse, logp, H; loss scalars.
 __global__ void __launch_bounds__(256) k_combine(TokenParams p) {
   // 64 tokens per block; wavefront w merges the vocabulary tiles k = w, w + 4, ... of its lane's
-  // token (loads coalesced over the 64 tokens), then the four partial results meet in LDS.
-  // Two passes: the maximum M of the tile maxima, then with w_k = e^{m_k - M}
-  //   S = sum_k w_k s_k,  T = sum_k w_k (u_k + (m_k - M) s_k),
-  // so that lse = M + ln S and sum_j p_j (z_j - lse) = T / S - ln S.
+  // token (loads coalesced over the 64 tokens) in one pass with a running maximum M_w:
+  //   S_w = sum_k e^{m_k - M_w} s_k,  T_w = sum_k e^{m_k - M_w} (u_k + (m_k - M_w) s_k),
+  // rescaled by e^{M_w - M'} (and T_w shifted by (M_w - M') S_w) whenever the maximum grows to M';
+  // the four wavefront results meet in LDS the same way.  Then lse = M + ln S and
+  // sum_j p_j (z_j - lse) = T / S - ln S.
   __shared__ float s_m[4][64];
   __shared__ double s_S[4][64], s_T[4][64];
   int64_t rc = (int64_t)p.hdr->n_eff - p.c0;
@@ -133,28 +134,42 @@ __global__ void __launch_bounds__(256) k_combine(TokenParams p) {
   const int64_t tl = (int64_t)blockIdx.x * 64 + lane;
   if ((int64_t)blockIdx.x * 64 >= rc) return;
   const bool act = tl < rc;
-  float mx = -INFINITY;
-  if (act)
-    for (int k = wv; k < p.nvt; k += 4) mx = fmaxf(mx, p.pm[(int64_t)k * p.Mc + tl]);
-  s_m[wv][lane] = mx;
-  __syncthreads();
-  const float M = fmaxf(fmaxf(s_m[0][lane], s_m[1][lane]), fmaxf(s_m[2][lane], s_m[3][lane]));
+  float Mw = -INFINITY;
   double S = 0.0, T = 0.0;
   if (act)
     for (int k = wv; k < p.nvt; k += 4) {
       const int64_t o = (int64_t)k * p.Mc + tl;
       const float mk = p.pm[o];
-      const double w = (double)__builtin_amdgcn_exp2f((mk - M) * kLog2e);
       const double sk = (double)p.ps[o];
+      const double uk = (double)p.pu[o];
+      if (mk > Mw) {
+        if (Mw > -INFINITY) {
+          const double f = (double)__builtin_amdgcn_exp2f((Mw - mk) * kLog2e);
+          T = f * (T + (double)(Mw - mk) * S);
+          S *= f;
+        }
+        Mw = mk;
+      }
+      const double w = (double)__builtin_amdgcn_exp2f((mk - Mw) * kLog2e);
       S += w * sk;
-      T += w * ((double)p.pu[o] + (double)(mk - M) * sk);
+      T += w * (uk + (double)(mk - Mw) * sk);
     }
+  s_m[wv][lane] = Mw;
   s_S[wv][lane] = S;
   s_T[wv][lane] = T;
   __syncthreads();
   if (wv != 0 || !act) return;
-  S = s_S[0][lane] + s_S[1][lane] + s_S[2][lane] + s_S[3][lane];
-  T = s_T[0][lane] + s_T[1][lane] + s_T[2][lane] + s_T[3][lane];
+  const float M = fmaxf(fmaxf(s_m[0][lane], s_m[1][lane]), fmaxf(s_m[2][lane], s_m[3][lane]));
+  S = 0.0;
+  T = 0.0;
+#pragma unroll
+  for (int w4 = 0; w4 < 4; ++w4) {
+    const float mw = s_m[w4][lane];
+    if (mw == -INFINITY) continue;  // a wavefront without vocabulary tiles (fewer than 4 tiles)
+    const double f = (double)__builtin_amdgcn_exp2f((mw - M) * kLog2e);
+    S += f * s_S[w4][lane];
+    T += f * (s_T[w4][lane] + (double)(mw - M) * s_S[w4][lane]);
+  }
   const int64_t i = p.c0 + tl;
   const double lnS = log(S);
   const double lse = (double)M + lnS;
