@@ -60,9 +60,9 @@ __device__ __forceinline__ u32x4 vpack(const T* e) {
   return v;
 }
 
-// ---- W^T [d][Vp] (zero rows beyond V) for the dhidden GEMM, 64 x 64 tiles through LDS.
+// ---- W^T [d][ldw] (columns v < Vp; zero beyond V) for the dhidden GEMM, 64 x 64 tiles through LDS.
 template <typename T>
-__global__ void __launch_bounds__(256) k_transpose_w(const T* W, T* WT, int V, int64_t Vp, int d) {
+__global__ void __launch_bounds__(256) k_transpose_w(const T* W, T* WT, int V, int64_t Vp, int d, int64_t ldw) {
   __shared__ T tile[64][65];
   const int64_t v0 = (int64_t)blockIdx.x * 64;
   const int j0 = blockIdx.y * 64;
@@ -75,15 +75,16 @@ __global__ void __launch_bounds__(256) k_transpose_w(const T* W, T* WT, int V, i
   __syncthreads();
   for (int e = threadIdx.x; e < 64 * 64; e += 256) {
     const int r = e >> 6, c = e & 63;   // r: feature, c: vocabulary
-    if (j0 + r < d && v0 + c < Vp) WT[(int64_t)(j0 + r) * Vp + v0 + c] = tile[c][r];
+    if (j0 + r < d && v0 + c < Vp) WT[(int64_t)(j0 + r) * ldw + v0 + c] = tile[c][r];
   }
 }
 
-// ---- Hc[t][:] = hidden[idx[c0 + t]][:] and HT[j][t] (zero columns t >= rows, up to the K pad).
+// ---- Hc[t][:] = hidden[idx[c0 + t]][:] and HT[j][t] (row stride ldt; zero columns t >= rows, up to
+// the K pad).
 template <typename T>
 __global__ void __launch_bounds__(256)
 k_gather(const T* hidden, int d, const int32_t* idx, const WsHeader* hdr, int64_t c0, int64_t Mc, T* hc, T* ht,
-         int want_ht) {
+         int64_t ldt, int want_ht) {
   constexpr int EPC = 16 / sizeof(T);     // elements per 16-byte chunk
   constexpr int CPR = 64 / EPC;           // chunks per 64-feature row slice
   __shared__ __attribute__((aligned(16))) T tile[64][64 + EPC];
@@ -114,7 +115,7 @@ k_gather(const T* hidden, int d, const int32_t* idx, const WsHeader* hdr, int64_
     T vals[EPC];
 #pragma unroll
     for (int i = 0; i < EPC; ++i) vals[i] = tile[ch * EPC + i][jl];
-    *reinterpret_cast<u32x4*>(ht + (int64_t)j * Mc + t0 + ch * EPC) = vpack<T>(vals);
+    *reinterpret_cast<u32x4*>(ht + (int64_t)j * ldt + t0 + ch * EPC) = vpack<T>(vals);
   }
 }
 
@@ -270,7 +271,7 @@ __global__ void __launch_bounds__(256) k_dz(DzParams p) {
     u32x4 raw[EPC];
 #pragma unroll
     for (int j = 0; j < EPC; ++j)
-      raw[j] = *reinterpret_cast<const u32x4*>(q + (t0 + tg * EPC + j) * p.Vp + v0 + vl0);
+      raw[j] = *reinterpret_cast<const u32x4*>(q + (t0 + tg * EPC + j) * p.ldq + v0 + vl0);
     float o[EPC][EPC];
 #pragma unroll
     for (int j = 0; j < EPC; ++j) {
@@ -291,14 +292,14 @@ __global__ void __launch_bounds__(256) k_dz(DzParams p) {
       T row[EPC];
 #pragma unroll
       for (int k = 0; k < EPC; ++k) row[k] = to_storage<T>(o[j][k]);
-      *reinterpret_cast<u32x4*>(q + (t0 + tg * EPC + j) * p.Vp + v0 + vl0) = vpack<T>(row);
+      *reinterpret_cast<u32x4*>(q + (t0 + tg * EPC + j) * p.ldq + v0 + vl0) = vpack<T>(row);
     }
 #pragma unroll
     for (int k = 0; k < EPC; ++k) {
       T col[EPC];
 #pragma unroll
       for (int j = 0; j < EPC; ++j) col[j] = to_storage<T>(o[j][k]);
-      *reinterpret_cast<u32x4*>(dzt + (v0 + vl0 + k) * p.Mc + t0 + tg * EPC) = vpack<T>(col);
+      *reinterpret_cast<u32x4*>(dzt + (v0 + vl0 + k) * p.ldt + t0 + tg * EPC) = vpack<T>(col);
     }
   }
 }
@@ -435,26 +436,27 @@ k_zero_fill(const uint8_t* keep, int64_t N, int d, T* dh, float* o1, float* o2, 
 
 }  // namespace
 
-hipError_t launch_transpose_w(int dtype, const void* W, void* WT, int V, int64_t Vp, int d, hipStream_t s) {
+hipError_t launch_transpose_w(int dtype, const void* W, void* WT, int V, int64_t Vp, int d, int64_t ldw,
+                              hipStream_t s) {
   dim3 grid((unsigned)(Vp / 64), (unsigned)((d + 63) / 64));
   prof_mark(KK_TRANSPOSE_W, true, s);
   if (dtype == RLK_DTYPE_BF16)
-    k_transpose_w<uint16_t><<<grid, 256, 0, s>>>((const uint16_t*)W, (uint16_t*)WT, V, Vp, d);
+    k_transpose_w<uint16_t><<<grid, 256, 0, s>>>((const uint16_t*)W, (uint16_t*)WT, V, Vp, d, ldw);
   else
-    k_transpose_w<float><<<grid, 256, 0, s>>>((const float*)W, (float*)WT, V, Vp, d);
+    k_transpose_w<float><<<grid, 256, 0, s>>>((const float*)W, (float*)WT, V, Vp, d, ldw);
   prof_mark(KK_TRANSPOSE_W, false, s);
   return hipGetLastError();
 }
 
 hipError_t launch_gather(int dtype, const void* hidden, int d, const int32_t* idx, const WsHeader* hdr, int64_t c0,
-                         int64_t Mc, void* hc, void* ht, bool want_ht, hipStream_t s) {
+                         int64_t Mc, void* hc, void* ht, int64_t ldt, bool want_ht, hipStream_t s) {
   dim3 grid((unsigned)(Mc / 64), (unsigned)((d + 63) / 64));
   prof_mark(KK_GATHER, true, s);
   if (dtype == RLK_DTYPE_BF16)
     k_gather<uint16_t><<<grid, 256, 0, s>>>((const uint16_t*)hidden, d, idx, hdr, c0, Mc, (uint16_t*)hc,
-                                            (uint16_t*)ht, want_ht ? 1 : 0);
+                                            (uint16_t*)ht, ldt, want_ht ? 1 : 0);
   else
-    k_gather<float><<<grid, 256, 0, s>>>((const float*)hidden, d, idx, hdr, c0, Mc, (float*)hc, (float*)ht,
+    k_gather<float><<<grid, 256, 0, s>>>((const float*)hidden, d, idx, hdr, c0, Mc, (float*)hc, (float*)ht, ldt,
                                          want_ht ? 1 : 0);
   prof_mark(KK_GATHER, false, s);
   return hipGetLastError();
