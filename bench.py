@@ -298,6 +298,104 @@ def stats_summary(stats_csv, title, cmd):
     return "\n".join(out) + "\n"
 
 
+def next_rows(cfg, inp, params, steps):
+    """Timings of the adjacent paths at the workload's shape: the loss call with truncated
+    importance sampling and the KL term switched on (overhead over the plain call); the PPO path's
+    GAE, value loss and linear value head (time and achieved bandwidth on their algorithmic
+    bytes); the host prefix-tree packer on a synthetic call log."""
+    import numpy as np
+    import torch
+
+    import paper_2608_16798_amd as rlk
+
+    st = inp["st"]
+    N, R, d = st.N, st.R, cfg.d
+    n_eff = int(np.asarray(st.mask, dtype=np.int64).sum())
+    esz = 2 if cfg.dtype == "bf16" else 4
+    dev = "cuda"
+    g = torch.Generator(device=dev).manual_seed(cfg.seed + 4242)
+    loss = torch.empty(1, dtype=torch.float32, device=dev)
+    dh = torch.empty_like(inp["h"])
+    dW = torch.empty(inp["W"].shape, dtype=torch.float32, device=dev)
+    batch = rlk.make_batch(inp["h"], inp["W"], inp["cu"])
+    pk = rlk.make_params(eps_low=params.eps_low, eps_high=params.eps_high, tis_cap=2.0, kl_coef=0.05)
+    ws = rlk.alloc_workspace(max(rlk.workspace_size(batch, params), rlk.workspace_size(batch, pk)), dev)
+    rollout = inp["old"] + 0.1 * torch.randn(N, generator=g, device=dev)
+    ref = inp["old"] + 0.2 * torch.randn(N, generator=g, device=dev)
+
+    def timed(fn, reps):
+        fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / reps
+
+    def loss_call(p, **kw):
+        return lambda: rlk.pg_loss_fwd_bwd(inp["h"], inp["W"], inp["targets"], inp["mask"], inp["cu"], inp["old"],
+                                           inp["rewards"], inp["gid"], p, loss=loss, dhidden=dh, dW=dW, ws=ws, **kw)
+
+    out = {"workload": cfg.name, "N": N, "N_eff": n_eff}
+    base = timed(loss_call(params), steps)
+    tk = timed(loss_call(pk, rollout_logp=rollout, ref_logp=ref), steps)
+    out["loss_call_ms"] = round(base, 3)
+    out["loss_call_tis_kl_ms"] = round(tk, 3)
+    # PPO path
+    values = torch.randn(N, generator=g, device=dev)
+    adv = torch.empty(N, dtype=torch.float32, device=dev)
+    ret = torch.empty(N, dtype=torch.float32, device=dev)
+    t_gae = timed(lambda: rlk.gae(values, inp["rewards"], inp["mask"], inp["cu"], inp["gid"], adv=adv, returns=ret), 20)
+    vws = rlk.alloc_workspace(rlk.value_workspace_size(R), dev)
+    vl = torch.empty(1, dtype=torch.float32, device=dev)
+    dv = torch.empty(N, dtype=torch.float32, device=dev)
+    t_vl = timed(lambda: rlk.value_loss(values, ret, inp["mask"], inp["cu"], inp["gid"], loss=vl, dvalues=dv,
+                                        ws=vws), 20)
+    w_v = (0.02 * torch.randn(d, generator=g, device=dev)).to(inp["h"].dtype)
+    vals = torch.empty(N, dtype=torch.float32, device=dev)
+    t_hf = timed(lambda: rlk.value_head_fwd(inp["h"], w_v, 0.1, inp["mask"], inp["cu"], inp["gid"], values=vals), 20)
+    hws = rlk.alloc_workspace(rlk.value_head_workspace_size(inp["h"], inp["cu"]), dev)
+    dhv = torch.empty_like(inp["h"])
+    dwv = torch.empty(d, dtype=torch.float32, device=dev)
+    dbv = torch.empty(1, dtype=torch.float32, device=dev)
+    t_hb = timed(lambda: rlk.value_head_bwd(inp["h"], w_v, inp["mask"], inp["cu"], inp["gid"], dv, dhidden=dhv,
+                                            dw_v=dwv, db_v=dbv, ws=hws), 20)
+    rate = lambda b, ms: round(b / (ms * 1e-3) / 1e12, 2)
+    out["gae_ms"] = round(t_gae, 4)
+    out["value_loss_ms"] = round(t_vl, 4)
+    out["value_head_fwd_ms"] = round(t_hf, 4)
+    out["value_head_fwd_TBps"] = rate(n_eff * d * esz, t_hf)          # read the policy rows
+    out["value_head_bwd_ms"] = round(t_hb, 4)
+    out["value_head_bwd_TBps"] = rate(N * d * esz + n_eff * d * esz, t_hb)  # read policy rows, write all rows
+    # host prefix-tree packer: 128 rollouts of 8 calls; each call's context is the previous history
+    # (prompt, responses, tool observations), and every fourth rollout repeats one call
+    rng = np.random.default_rng(cfg.seed + 77)
+    calls_per_rollout, n_tok = [], 0
+    for r in range(128):
+        hist = list(rng.integers(0, cfg.V, 512))
+        calls = []
+        for c in range(8):
+            resp = list(rng.integers(0, cfg.V, 256))
+            calls.append((np.asarray(hist, dtype=np.int32), np.asarray(resp, dtype=np.int32)))
+            n_tok += len(hist) + len(resp)
+            if r % 4 == 0 and c == 3:
+                calls.append(calls[-1])
+                n_tok += len(hist) + len(resp)
+            hist = hist + resp + list(rng.integers(0, cfg.V, 64))
+        calls_per_rollout.append(calls)
+    t0 = time.perf_counter()
+    packed = rlk.tree_pack(calls_per_rollout)
+    dt = time.perf_counter() - t0
+    out["tree_pack_calls_tokens"] = n_tok
+    out["tree_pack_positions"] = int(len(packed["token"]))
+    out["tree_pack_rows"] = int(len(packed["row_target"]))
+    out["tree_pack_s"] = round(dt, 4)
+    out["tree_pack_input_tokens_per_s"] = round(n_tok / dt, 1)
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -308,6 +406,8 @@ def main():
                     help="keep 1/K of the workload's groups: one GPU's share of a K-GPU data-parallel step")
     ap.add_argument("--chunk-rows", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--next-rows", action="store_true",
+                    help="time the adjacent paths (TIS/KL options, GAE, value loss, value head, tree packing) and exit")
     ap.add_argument("--graph", action="store_true",
                     help="capture one step as a HIP graph and replay it (launch-bound workloads); no per-kernel events")
     ap.add_argument("--cpu-tokens", type=int, default=1024)
@@ -403,6 +503,10 @@ def main():
         raise SystemExit("device data error in the benchmark batch")
     s = rlk.stats_from_tensor(stats)
     n_eff = int(s["n_policy_tokens"])
+
+    if args.next_rows:
+        print(json.dumps(next_rows(cfg, inp, params, args.steps)), flush=True)
+        return
 
     run = step
     if args.graph:

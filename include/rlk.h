@@ -229,7 +229,7 @@ rlk_status_t rlk_value_head_fwd(const rlk_batch_t* b, const void* hidden, const 
  * computes, dhidden[t] = dvalues[t] w_v, added to dhidden when accumulate = 1 (other rows then
  * untouched) and written otherwise (other rows then set to 0); dhidden may be NULL (skipped).
  * dw_v [d] f32 = sum_t dvalues[t] hidden[t] and db_v [1] f32 = sum_t dvalues[t] over those rows,
- * from per-1024-row partial sums added in row order (deterministic).  ws:
+ * from per-256-row partial sums added in row order (deterministic).  ws:
  * rlk_value_head_workspace_size bytes, 256-byte aligned. */
 rlk_status_t rlk_value_head_workspace_size(const rlk_batch_t* b, size_t* bytes);
 rlk_status_t rlk_value_head_bwd(const rlk_batch_t* b, const void* hidden, const void* w_v, const uint8_t* mask,

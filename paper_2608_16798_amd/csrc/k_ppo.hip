@@ -214,7 +214,7 @@ __device__ __forceinline__ uint32_t bf16_pair(float lo, float hi) {
   return (uint32_t)__builtin_bit_cast(uint16_t, (__bf16)lo) | ((uint32_t)__builtin_bit_cast(uint16_t, (__bf16)hi) << 16);
 }
 
-constexpr int kHeadRows = 1024;   // rows per workgroup of the dW partial sums
+constexpr int kHeadRows = 256;    // rows per workgroup of the dW partial sums
 
 // one wavefront per row
 template <typename T>
@@ -247,14 +247,15 @@ k_value_head_fwd(int64_t N, int d, const T* h, const T* w, float b, const uint8_
 template <typename T>
 __global__ void __launch_bounds__(256)
 k_value_head_dh(int64_t N, int d, const T* w, const float* dv, const uint8_t* mask, const int32_t* cu,
-                const int32_t* gid, int R, T* dh, int accumulate) {
+                const int32_t* gid, int R, T* dh, int accumulate, float* gk) {
   constexpr int EPC = 16 / sizeof(T);
   const int64_t t = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
   if (t >= N) return;
   const bool keep = kept_row(mask, cu, gid, R, t);
-  if (!keep && accumulate) return;
   const float g = keep ? dv[t] : 0.0f;
+  if (lane == 0) gk[t] = g;  // the row's gradient for the dw / db sums
+  if (!dh || (!keep && accumulate)) return;
   T* row = dh + t * d;
   for (int c = lane; c < d / EPC; c += 64) {
     float y[EPC], o[EPC];
@@ -281,29 +282,38 @@ k_value_head_dh(int64_t N, int d, const T* w, const float* dv, const uint8_t* ma
 // order), part_db[blk] = sum_t dV_t (fp64); each thread owns 16-byte column chunks.
 template <typename T>
 __global__ void __launch_bounds__(256)
-k_value_head_dw_partial(int64_t N, int d, const T* h, const float* dv, const uint8_t* mask, const int32_t* cu,
-                        const int32_t* gid, int R, float* part, double* part_db) {
+k_value_head_dw_partial(int64_t N, int d, const T* h, const float* gk, float* part, double* part_db) {
   constexpr int EPC = 16 / sizeof(T);
   const int64_t t0 = (int64_t)blockIdx.x * kHeadRows, t1 = min(N, t0 + kHeadRows);
-  const int r0 = R > 0 ? rollout_of_row(cu, R, t0) : 0;
   for (int cb = 0; cb < d / EPC; cb += 256) {
     const int c = cb + threadIdx.x;
     float acc[EPC];
 #pragma unroll
     for (int e = 0; e < EPC; ++e) acc[e] = 0.0f;
     double db = 0.0;
-    int r = r0;
-    for (int64_t t = t0; t < t1; ++t) {
-      while (r < R - 1 && (int64_t)cu[r + 1] <= t) ++r;
-      const bool keep = (!mask || mask[t]) && (!gid || gid[r] >= 0);
-      const float g = keep ? dv[t] : 0.0f;
-      if (g == 0.0f) continue;
-      db += (double)g;
-      if (c < d / EPC) {
-        float x[EPC];
-        unpack8<T>(*reinterpret_cast<const u32x4*>(h + t * d + c * EPC), x);
+    // rows in groups of four: the row loads of a group are issued together (skipped for rows with
+    // no gradient), then accumulated in row order
+    for (int64_t t = t0; t < t1; t += 4) {
+      float g4[4];
+      u32x4 x4[4];
 #pragma unroll
-        for (int e = 0; e < EPC; ++e) acc[e] = fmaf(g, x[e], acc[e]);
+      for (int u = 0; u < 4; ++u) {
+        const int64_t tt = t + u;
+        g4[u] = 0.0f;
+        x4[u] = u32x4{0, 0, 0, 0};
+        if (tt < t1) {
+          g4[u] = gk[tt];
+          if (g4[u] != 0.0f && c < d / EPC) x4[u] = *reinterpret_cast<const u32x4*>(h + tt * d + c * EPC);
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        if (g4[u] == 0.0f) continue;
+        db += (double)g4[u];
+        float x[EPC];
+        unpack8<T>(x4[u], x);
+#pragma unroll
+        for (int e = 0; e < EPC; ++e) acc[e] = fmaf(g4[u], x[e], acc[e]);
       }
     }
     if (c < d / EPC) {
@@ -314,19 +324,32 @@ k_value_head_dw_partial(int64_t N, int d, const T* h, const float* dv, const uin
   }
 }
 
-// final sums over the workgroup partials, in workgroup order (fp64)
+// final sums over the workgroup partials in a fixed order (fp64): a block owns 32 columns; thread
+// (column, part) adds the partials of its eighth of the workgroups in workgroup order, then the
+// eight part sums of a column are added in part order.
 __global__ void __launch_bounds__(256)
 k_value_head_dw_final(int nblk, int d, const float* part, const double* part_db, float* dw, float* dbias) {
-  const int j = blockIdx.x * 256 + threadIdx.x;
+  __shared__ double sh[8][32];
+  const int col = threadIdx.x & 31, pt = threadIdx.x >> 5;
+  const int j = blockIdx.x * 32 + col;
+  const int b0 = (int)((int64_t)nblk * pt / 8), b1 = (int)((int64_t)nblk * (pt + 1) / 8);
+  double s = 0.0;
   if (j < d) {
-    double s = 0.0;
-    for (int b = 0; b < nblk; ++b) s += (double)part[(int64_t)b * d + j];
-    dw[j] = (float)s;
+#pragma unroll 8
+    for (int b = b0; b < b1; ++b) s += (double)part[(int64_t)b * d + j];
+  }
+  sh[pt][col] = s;
+  __syncthreads();
+  if (pt == 0 && j < d) {
+    double t = 0.0;
+#pragma unroll
+    for (int q = 0; q < 8; ++q) t += sh[q][col];
+    dw[j] = (float)t;
   }
   if (blockIdx.x == 0 && threadIdx.x == 0) {
-    double s = 0.0;
-    for (int b = 0; b < nblk; ++b) s += part_db[b];
-    dbias[0] = (float)s;
+    double t = 0.0;
+    for (int b = 0; b < nblk; ++b) t += part_db[b];
+    dbias[0] = (float)t;
   }
 }
 
@@ -334,7 +357,7 @@ k_value_head_dw_final(int nblk, int d, const float* part, const double* part_db,
 
 size_t value_head_workspace(int64_t N, int d) {
   const int64_t nblk = (N + kHeadRows - 1) / kHeadRows;
-  return (size_t)(((nblk * d * 4 + 255) / 256) * 256 + ((nblk * 8 + 255) / 256) * 256);
+  return (size_t)(((nblk * d * 4 + 255) / 256) * 256 + ((nblk * 8 + 255) / 256) * 256 + ((N * 4 + 255) / 256) * 256);
 }
 
 hipError_t launch_value_head_fwd(int dtype, int64_t N, int d, int R, const void* h, const void* w, float b,
@@ -360,26 +383,27 @@ hipError_t launch_value_head_bwd(int dtype, int64_t N, int d, int R, const void*
   const int64_t nblk64 = (N + kHeadRows - 1) / kHeadRows;
   const int nblk = (int)nblk64;
   float* part = reinterpret_cast<float*>(ws);
-  double* part_db = reinterpret_cast<double*>(ws + ((nblk64 * d * 4 + 255) / 256) * 256);
+  const size_t part_bytes = ((nblk64 * d * 4 + 255) / 256) * 256;
+  double* part_db = reinterpret_cast<double*>(ws + part_bytes);
+  float* gk = reinterpret_cast<float*>(ws + part_bytes + ((nblk64 * 8 + 255) / 256) * 256);
   const bool bf = dtype == RLK_DTYPE_BF16;
-  if (dh && N > 0) {
+  if (N > 0) {
+    // dhidden rows (when dh is given) and every row's gradient gk for the sums below
     const unsigned grid = (unsigned)((N + 3) / 4);
     if (bf)
       k_value_head_dh<bf16_t><<<grid, 256, 0, s>>>(N, d, (const bf16_t*)w, dv, mask, cu, gid, R, (bf16_t*)dh,
-                                                   accumulate);
+                                                   accumulate, gk);
     else
       k_value_head_dh<float><<<grid, 256, 0, s>>>(N, d, (const float*)w, dv, mask, cu, gid, R, (float*)dh,
-                                                  accumulate);
+                                                  accumulate, gk);
   }
   if (nblk > 0) {
     if (bf)
-      k_value_head_dw_partial<bf16_t><<<nblk, 256, 0, s>>>(N, d, (const bf16_t*)h, dv, mask, cu, gid, R, part,
-                                                           part_db);
+      k_value_head_dw_partial<bf16_t><<<nblk, 256, 0, s>>>(N, d, (const bf16_t*)h, gk, part, part_db);
     else
-      k_value_head_dw_partial<float><<<nblk, 256, 0, s>>>(N, d, (const float*)h, dv, mask, cu, gid, R, part,
-                                                          part_db);
+      k_value_head_dw_partial<float><<<nblk, 256, 0, s>>>(N, d, (const float*)h, gk, part, part_db);
   }
-  k_value_head_dw_final<<<(unsigned)((d + 255) / 256), 256, 0, s>>>(nblk, d, part, part_db, dw, dbias);
+  k_value_head_dw_final<<<(unsigned)((d + 31) / 32), 256, 0, s>>>(nblk, d, part, part_db, dw, dbias);
   prof_mark(KK_VALUE_HEAD, false, s);
   return hipGetLastError();
 }
