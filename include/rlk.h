@@ -13,7 +13,8 @@
  * Conventions shared by every entry point
  *   - Every tensor pointer is a DEVICE pointer unless stated otherwise; row-major layout.
  *   - hidden [N, d], W [V, d] and dhidden [N, d] use the batch dtype (fp32 or bf16).
- *     Rows must be 16-byte aligned: d must be a multiple of 8.
+ *     Their base pointers and rows must be 16-byte aligned: d must be a multiple of 8
+ *     (a misaligned pointer is rejected with RLK_EINVAL).
  *   - targets[t] is the token sampled at position t, already aligned with hidden[t] (no
  *     shift inside); on policy rows it must lie in [0, V); on other rows it is ignored.
  *   - mask[t] = 1 marks a policy-generated token (trained); 0 marks harness/tool tokens.

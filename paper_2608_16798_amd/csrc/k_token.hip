@@ -60,22 +60,42 @@ __device__ __forceinline__ u32x4 vpack(const T* e) {
   return v;
 }
 
-// ---- W^T [d][ldw] (columns v < Vp; zero beyond V) for the dhidden GEMM, 64 x 64 tiles through LDS.
+// ---- W^T [d][ldw] (columns v < Vp; zero beyond V) for the dhidden GEMM, 64 x 64 tiles through LDS
+// with 16-byte global loads and stores: a thread reads 16 bytes along a row of W and writes 16
+// bytes (EPC consecutive vocabulary entries) along a row of W^T.
 template <typename T>
 __global__ void __launch_bounds__(256) k_transpose_w(const T* W, T* WT, int V, int64_t Vp, int d, int64_t ldw) {
-  __shared__ T tile[64][65];
+  constexpr int EPC = 16 / sizeof(T);
+  constexpr int CPR = 64 / EPC;  // 16-byte chunks per 64-element tile row
+  __shared__ T tile[64][64 + 2];
   const int64_t v0 = (int64_t)blockIdx.x * 64;
   const int j0 = blockIdx.y * 64;
-  for (int e = threadIdx.x; e < 64 * 64; e += 256) {
-    const int r = e >> 6, c = e & 63;
-    T val = 0;
-    if (v0 + r < V && j0 + c < d) val = W[(v0 + r) * d + j0 + c];
-    tile[r][c] = val;
+  for (int c = threadIdx.x; c < 64 * CPR; c += 256) {
+    const int r = c / CPR, ch = c % CPR;  // vocabulary row r, feature chunk ch
+    const int64_t v = v0 + r;
+    const int j = j0 + ch * EPC;
+    T vals[EPC];
+    if (v < V && j + EPC <= d) {
+      const u32x4 x = *reinterpret_cast<const u32x4*>(W + v * d + j);
+#pragma unroll
+      for (int e = 0; e < EPC; ++e) vals[e] = reinterpret_cast<const T*>(&x)[e];
+    } else {
+#pragma unroll
+      for (int e = 0; e < EPC; ++e) vals[e] = (v < V && j + e < d) ? W[v * d + j + e] : T(0);
+    }
+#pragma unroll
+    for (int e = 0; e < EPC; ++e) tile[r][ch * EPC + e] = vals[e];
   }
   __syncthreads();
-  for (int e = threadIdx.x; e < 64 * 64; e += 256) {
-    const int r = e >> 6, c = e & 63;   // r: feature, c: vocabulary
-    if (j0 + r < d && v0 + c < Vp) WT[(int64_t)(j0 + r) * ldw + v0 + c] = tile[c][r];
+  for (int c = threadIdx.x; c < 64 * CPR; c += 256) {
+    const int jr = c / CPR, ch = c % CPR;  // feature row jr of W^T, vocabulary chunk ch
+    const int j = j0 + jr;
+    const int64_t v = v0 + ch * EPC;
+    if (j >= d || v >= Vp) continue;
+    T vals[EPC];
+#pragma unroll
+    for (int e = 0; e < EPC; ++e) vals[e] = tile[ch * EPC + e][jr];
+    *reinterpret_cast<u32x4*>(WT + (int64_t)j * ldw + v) = vpack<T>(vals);
   }
 }
 

@@ -47,6 +47,8 @@ rlk_status_t report_error(rlk_status_t code, const char* msg) { return fail(code
 namespace {
 
 inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+// Row tensors (hidden, W, dhidden) are read and written with 16-byte vector accesses.
+inline bool misaligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) != 0; }
 inline int64_t roundup(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
 
 struct Alloc {
@@ -292,6 +294,7 @@ rlk_status_t rlk_logprob_fwd(const rlk_batch_t* b, const void* hidden, const voi
   if (st) return st;
   if (b->N > 0 && (!hidden || !targets || !logp)) return fail(RLK_EINVAL, "hidden, targets or logp is NULL");
   if (!W) return fail(RLK_EINVAL, "W is NULL");
+  if (misaligned16(hidden) || misaligned16(W)) return fail(RLK_EINVAL, "hidden and W must be 16-byte aligned");
   WsLayout L;
   st = layout(b, false, 0, L);
   if (st) return st;
@@ -424,6 +427,8 @@ rlk_status_t rlk_pg_loss_fwd_bwd(const rlk_batch_t* b, const void* hidden, const
   if (!W || !dW || !loss) return fail(RLK_EINVAL, "W, dW or loss is NULL");
   if (b->N > 0 && (!hidden || !targets || !old_logp || !dhidden))
     return fail(RLK_EINVAL, "hidden, targets, old_logp or dhidden is NULL");
+  if (misaligned16(hidden) || misaligned16(W) || misaligned16(dhidden))
+    return fail(RLK_EINVAL, "hidden, W and dhidden must be 16-byte aligned");
   if (b->R > 0 && (!rewards || !group_ids)) return fail(RLK_EINVAL, "rewards or group_ids is NULL");
   if (!(p->eps_low >= 0.0f && p->eps_low < 1.0f) || !(p->eps_high >= 0.0f) || !isfinite(p->eps_high))
     return fail(RLK_EINVAL, "clip range must satisfy 0 <= eps_low < 1 and finite eps_high >= 0");
@@ -672,6 +677,7 @@ rlk_status_t rlk_value_head_fwd(const rlk_batch_t* b, const void* hidden, const 
   if (st) return st;
   if (!isfinite(b_v)) return fail(RLK_EINVAL, "b_v must be finite");
   if (b->N > 0 && (!hidden || !w_v || !values)) return fail(RLK_EINVAL, "hidden, w_v or values is NULL");
+  if (misaligned16(hidden)) return fail(RLK_EINVAL, "hidden must be 16-byte aligned");
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   RLK_TRY(launch_value_head_fwd(b->dtype, b->N, b->d, b->R, hidden, w_v, b_v, mask, b->cu_seqlens, group_ids,
                                 values, s),
@@ -687,6 +693,8 @@ rlk_status_t rlk_value_head_bwd(const rlk_batch_t* b, const void* hidden, const 
   if (accumulate != 0 && accumulate != 1) return fail(RLK_EINVAL, "accumulate must be 0 or 1");
   if (!dw_v || !db_v) return fail(RLK_EINVAL, "dw_v or db_v is NULL");
   if (b->N > 0 && (!hidden || !w_v || !dvalues)) return fail(RLK_EINVAL, "hidden, w_v or dvalues is NULL");
+  if (misaligned16(hidden) || misaligned16(dhidden))
+    return fail(RLK_EINVAL, "hidden and dhidden must be 16-byte aligned");
   st = check_ws(ws, ws_bytes, value_head_workspace(b->N, b->d));
   if (st) return st;
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);

@@ -101,6 +101,11 @@ def test_host_validation(lib):
         == rlk.RLK_EWORKSPACE
     assert lib.rlk_logprob_fwd(ctypes.byref(b), None, fake, fake, None, fake, None, None, fake, need, None) \
         == rlk.RLK_EINVAL
+    # row tensors must be 16-byte aligned (they are moved in 16-byte vectors)
+    assert lib.rlk_logprob_fwd(ctypes.byref(b), fake + 8, fake, fake, None, fake, None, None, fake, 256, None) \
+        == rlk.RLK_EINVAL
+    assert lib.rlk_logprob_fwd(ctypes.byref(b), fake, fake + 4, fake, None, fake, None, None, fake, 256, None) \
+        == rlk.RLK_EINVAL
     # loss parameters
     args = lambda p: (ctypes.byref(b), fake, fake, fake, None, fake, fake, fake, ctypes.byref(p), fake, fake, fake,
                       None, None, None, fake, 1 << 40, None)
@@ -155,6 +160,14 @@ def test_host_validation(lib):
     p = rlk.make_params()
     p.accumulate_dW = 2
     assert lib.rlk_pg_loss_fwd_bwd(*args(p)) == rlk.RLK_EINVAL
+    p = rlk.make_params()
+    for pos in (1, 2, 10):  # hidden, W, dhidden
+        a = list(args(p))
+        a[pos] = fake + 8
+        a[16] = 256  # a short workspace too: nothing can be launched if the check were missing
+        assert lib.rlk_pg_loss_fwd_bwd(*a) == rlk.RLK_EINVAL, pos
+    assert lib.rlk_value_head_fwd(ctypes.byref(hb), fake + 2, fake, ctypes.c_float(0.0), None, None, fake,
+                                  None) == rlk.RLK_EINVAL
     assert lib.rlk_group_advantage(8, fake, fake, ctypes.c_float(-1.0), fake, None, None, fake, 1 << 20, None) \
         == rlk.RLK_EINVAL
     assert lib.rlk_group_advantage(8, None, fake, ctypes.c_float(1e-6), fake, None, None, fake, 1 << 20, None) \
