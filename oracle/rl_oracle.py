@@ -137,10 +137,6 @@ def group_advantage(rewards, group_ids, adv_eps=1e-6):
 # --------------------------------------------------------------------------
 # Log-prob forward (Sec. 3.2.4) with full-row logits.
 # --------------------------------------------------------------------------
-def _logits(h_rows, W):
-    return _f64(h_rows) @ _f64(W).T
-
-
 def token_logprob(h_rows, W, y, block: int = 256, temperature: float = 1.0):
     """log pi(y_t | s_t), entropy and log-partition per row, from complete logit rows.
 

@@ -743,3 +743,70 @@ def test_temperature_gradients_match_finite_differences():
     rows = O.dw_rows(b["h"][idx], b["W"], np.arange(b["W"].shape[0]), b["targets"][idx], out["logp"], out["H"],
                      out["g"], out["e"], temperature=tau)
     np.testing.assert_allclose(rows, out["dW"], rtol=1e-10, atol=1e-14)
+
+
+# ---------------------- sampled_rows: the per-row checker of the full-size GPU parity tests
+def _sampled_rows_case(seed, agg, temperature):
+    b = _with_old_from_current(seed, sigma=0.5, excluded=(3,), per_group=(3, 4, 3))
+    b = _kink_safe(b, 0.2, 0.28, temperature=temperature)
+    rng = np.random.default_rng(seed + 7)
+    N = b["h"].shape[0]
+    b["rollout_logp"] = b["old_logp"] + rng.standard_normal(N) * 0.4   # TIS cap binds on part of the rows
+    b["ref_logp"] = b["old_logp"] + rng.standard_normal(N) * 0.3
+    kw = dict(eps_low=0.2, eps_high=0.28, entropy_coef=0.04, agg=agg, rollout_logp=b["rollout_logp"],
+              tis_cap=1.1, ref_logp=b["ref_logp"], kl_coef=0.07, temperature=temperature)
+    return b, kw
+
+
+@pytest.mark.parametrize("agg,temperature", [(O.AGG_SEQ, 1.0), (O.AGG_SEQ, 1.3), (O.AGG_TOKEN, 0.8)])
+def test_sampled_rows_reproduce_the_full_pass(agg, temperature):
+    # Sec. 2.3.1-2.3.2: a row's log-prob, entropy, chain-rule weights and dhidden depend only on the
+    # row and on its per-rollout scalars, so the row-restricted pass equals the full pass (itself
+    # pinned by finite differences and torch autograd) row by row, with every option switched on
+    b, kw = _sampled_rows_case(91, agg, temperature)
+    out = _loss(b, **kw)
+    assert 0 < out["clipped"].mean() < 1 and (out["tis"] < 1.1).any() and (out["tis"] == 1.1).any()
+    idx = out["idx"]
+    perm = np.random.default_rng(5).permutation(idx.shape[0])   # rows in any order and any block size
+    sel = idx[perm]
+    got = O.sampled_rows(b["h"][sel], b["W"], b["targets"][sel], b["old_logp"][sel], out["adv_tok"][perm],
+                         out["omega"][perm], eps_low=0.2, eps_high=0.28, entropy_coef=0.04,
+                         tis_rows=out["tis"][perm], ref_rows=b["ref_logp"][sel], kl_coef=0.07,
+                         temperature=temperature, block=5)
+    for k in ("lse", "logp", "H", "rho", "g", "e"):
+        np.testing.assert_allclose(got[k], out[k][perm], rtol=1e-12, atol=1e-15, err_msg=k)
+    np.testing.assert_array_equal(got["clipped"], out["clipped"][perm])
+    np.testing.assert_allclose(got["dh"], out["dh"][sel], rtol=1e-11, atol=1e-15)
+
+
+def test_sampled_rows_dhidden_matches_finite_differences_of_the_row_loss():
+    # independent of pg_loss_fwd_bwd: the row's loss term omega_t w_t (s_t + c H_t - beta KL_t) built
+    # from the log-softmax (pinned against torch.log_softmax) and differentiated numerically in h_t
+    tau = 1.3
+    b, kw = _sampled_rows_case(92, O.AGG_SEQ, tau)
+    out = _loss(b, grads=False, **kw)
+    idx = out["idx"]
+    pick = np.arange(0, idx.shape[0], max(1, idx.shape[0] // 6))
+    sel = idx[pick]
+    A, om, w = out["adv_tok"][pick], out["omega"][pick], out["tis"][pick]
+    got = O.sampled_rows(b["h"][sel], b["W"], b["targets"][sel], b["old_logp"][sel], A, om, eps_low=0.2,
+                         eps_high=0.28, entropy_coef=0.04, tis_rows=w, ref_rows=b["ref_logp"][sel], kl_coef=0.07,
+                         temperature=tau)
+
+    def row_loss(i, hrow):
+        _, lp, H = O.token_logprob(hrow[None, :], b["W"], b["targets"][sel[i]:sel[i] + 1], temperature=tau)
+        rho = math.exp(lp[0] - b["old_logp"][sel[i]])
+        s = min(rho * A[i], min(max(rho, 0.8), 1.28) * A[i])
+        r = b["ref_logp"][sel[i]] - lp[0]
+        kl = math.expm1(r) - r
+        return om[i] * w[i] * (s + 0.04 * H[0] - 0.07 * kl)
+
+    step = 1e-6
+    for i in range(sel.shape[0]):
+        h0 = b["h"][sel[i]].astype(np.float64)
+        for j in range(h0.shape[0]):
+            hp, hm = h0.copy(), h0.copy()
+            hp[j] += step
+            hm[j] -= step
+            fd = (row_loss(i, hp) - row_loss(i, hm)) / (2 * step)
+            assert abs(fd - got["dh"][i, j]) <= 1e-7 * max(1.0, abs(got["dh"][i]).max()), (i, j, fd, got["dh"][i, j])
