@@ -120,6 +120,68 @@ def _ptr(t) -> Optional[int]:
     return None if t is None else t.data_ptr()
 
 
+def _tensor(t, name: str, shape=None, dtypes=None, optional: bool = False, min_bytes: int = 0):
+    """Checks a tensor argument before its pointer crosses the C ABI: a torch tensor of one of
+    `dtypes`, of exactly `shape` (None entries match any size) and contiguous (row-major).
+    Raises TypeError / ValueError; nothing is launched.  Devices are checked afterwards, for all
+    arguments together, by _on_one_gpu."""
+    import torch
+
+    if t is None:
+        if optional:
+            return
+        raise ValueError(f"{name} is required")
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor, got {type(t).__name__}")
+    if dtypes is not None and t.dtype not in dtypes:
+        raise TypeError(f"{name} has dtype {t.dtype}, expected {' or '.join(str(d) for d in dtypes)}")
+    if shape is not None:
+        ok = t.dim() == len(shape) and all(w is None or int(a) == int(w) for a, w in zip(t.shape, shape))
+        if not ok:
+            want = "[" + ", ".join("*" if w is None else str(int(w)) for w in shape) + "]"
+            raise ValueError(f"{name} has shape {list(t.shape)}, expected {want}")
+    if min_bytes and t.numel() * t.element_size() < min_bytes:
+        raise ValueError(f"{name} holds {t.numel() * t.element_size()} bytes, needs at least {min_bytes}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous (row-major)")
+
+
+def _on_one_gpu(**tensors):
+    """Every given tensor (None entries skipped) lives on one and the same GPU."""
+    dev = None
+    for name, t in tensors.items():
+        if t is None:
+            continue
+        if not t.is_cuda:
+            raise ValueError(f"{name} must be a GPU tensor, got device {t.device}")
+        if dev is None:
+            dev = t.device
+        elif t.device != dev:
+            raise ValueError(f"{name} is on {t.device}, other arguments on {dev}")
+
+
+def _float_types():
+    import torch
+
+    return (torch.float32, torch.bfloat16)
+
+
+def _check_rows(hidden, W, targets, mask, cu_seqlens):
+    """The batch tensors shared by the log-prob and loss entry points; returns (N, d, V, R, device)."""
+    import torch
+
+    _tensor(hidden, "hidden", shape=(None, None), dtypes=_float_types())
+    N, d = hidden.shape
+    dev = hidden.device
+    _tensor(W, "W", shape=(None, d), dtypes=(hidden.dtype,))
+    _tensor(targets, "targets", shape=(N,), dtypes=(torch.int32,))
+    _tensor(mask, "mask", shape=(N,), dtypes=(torch.uint8, torch.bool), optional=True)
+    _tensor(cu_seqlens, "cu_seqlens", shape=(None,), dtypes=(torch.int32,))
+    if cu_seqlens.shape[0] < 1:
+        raise ValueError("cu_seqlens needs R + 1 >= 1 entries")
+    return N, d, W.shape[0], cu_seqlens.shape[0] - 1, dev
+
+
 def _stream_handle(stream) -> Optional[int]:
     import torch
 
@@ -181,7 +243,7 @@ def alloc_workspace(nbytes: int, device="cuda"):
     """A 256-byte aligned uint8 device buffer of at least nbytes (torch allocations are)."""
     import torch
 
-    ws = torch.empty(max(int(nbytes), 256), dtype=torch.uint8, device=device)
+    ws = torch.empty(max(int(nbytes), 256), dtype=torch.uint8ice)
     assert ws.data_ptr() % 256 == 0
     return ws
 
@@ -191,12 +253,18 @@ def logprob_fwd(hidden, W, targets, mask, cu_seqlens, logp=None, entropy=None, l
     """Per-token log-prob / entropy / log-partition of the sampled tokens (rows with mask 0 -> 0)."""
     import torch
 
+    N, d, V, R, dev = _check_rows(hidden, W, targets, mask, cu_seqlens)
+    f32 = (torch.float32,)
+    _tensor(logp, "logp", shape=(N,), dtypes=f32, optional=True)
+    _tensor(entropy, "entropy", shape=(N,), dtypes=f32, optional=True)
+    _tensor(lse, "lse", shape=(N,), dtypes=f32, optional=True)
+    _tensor(ws, "ws", dtypes=(torch.uint8,), optional=True)
+    _on_one_gpu(hidden=hidden, W=W, targets=targets, mask=mask, cu_seqlens=cu_seqlens, logp=logp, entropy=entropy,
+                lse=lse, ws=ws)
     lib = load_library()
     b = make_batch(hidden, W, cu_seqlens, temperature)
-    N = b.N
-    dev = hidden.device
     if logp is None:
-        logp = torch.empty(N, dtype=torch.float32, device=dev)
+        logp = torch.empty(N, dtype=torch.float32)
     if ws is None:
         ws = alloc_workspace(workspace_size(b), dev)
     _check(lib.rlk_logprob_fwd(ctypes.byref(b), _ptr(hidden), _ptr(W), _ptr(targets), _ptr(mask), _ptr(logp),
@@ -208,16 +276,24 @@ def compact(cu_seqlens, mask, group_ids=None, targets=None, N=None, V=1, d=8, ws
     """Compacted policy-token positions, their rollouts, per-rollout counts and N_eff (device tensors)."""
     import torch
 
-    lib = load_library()
+    _tensor(cu_seqlens, "cu_seqlens", shape=(None,), dtypes=(torch.int32,))
     dev = cu_seqlens.device
     R = cu_seqlens.shape[0] - 1
     if N is None:
+        if mask is None:
+            raise ValueError("compact needs N when mask is None")
         N = mask.shape[0]
+    _tensor(mask, "mask", shape=(N,), dtypes=(torch.uint8, torch.bool), optional=True)
+    _tensor(group_ids, "group_ids", shape=(R,), dtypes=(torch.int32,), optional=True)
+    _tensor(targets, "targets", shape=(N,), dtypes=(torch.int32,), optional=True)
+    _tensor(ws, "ws", dtypes=(torch.uint8,), optional=True)
+    _on_one_gpu(cu_seqlens=cu_seqlens, mask=mask, group_ids=group_ids, targets=targets, ws=ws)
+    lib = load_library()
     b = Batch(N=N, R=R, d=d, V=V, dtype=DTYPE_BF16, cu_seqlens=_ptr(cu_seqlens))
-    idx = torch.empty(max(N, 1), dtype=torch.int32, device=dev)
-    tokr = torch.empty(max(N, 1), dtype=torch.int32, device=dev)
-    n_pol = torch.empty(max(R, 1), dtype=torch.int32, device=dev)
-    n_eff = torch.empty(1, dtype=torch.int32, device=dev)
+    idx = torch.empty(max(N, 1), dtype=torch.int32)
+    tokr = torch.empty(max(N, 1), dtype=torch.int32)
+    n_pol = torch.empty(max(R, 1), dtype=torch.int32)
+    n_eff = torch.empty(1, dtype=torch.int32)
     if ws is None:
         ws = alloc_workspace(workspace_size(b), dev)
     _check(lib.rlk_compact(ctypes.byref(b), _ptr(mask), _ptr(group_ids), _ptr(targets), _ptr(idx), _ptr(tokr),
@@ -229,11 +305,18 @@ def group_advantage(rewards, group_ids, adv_eps=1e-6, adv=None, group_index=None
                     stream=None):
     import torch
 
-    lib = load_library()
+    _tensor(rewards, "rewards", shape=(None,), dtypes=(torch.float32,))
     R = rewards.shape[0]
     dev = rewards.device
+    _tensor(group_ids, "group_ids", shape=(R,), dtypes=(torch.int32,))
+    _tensor(adv, "adv", shape=(R,), dtypes=(torch.float32,), optional=True)
+    _tensor(group_index, "group_index", shape=(R,), dtypes=(torch.int32,), optional=True)
+    _tensor(n_groups, "n_groups", shape=(None,), dtypes=(torch.int32,), optional=True, min_bytes=4)
+    _tensor(ws, "ws", dtypes=(torch.uint8,), optional=True)
+    _on_one_gpu(rewards=rewards, group_ids=group_ids, adv=adv, group_index=group_index, n_groups=n_groups, ws=ws)
+    lib = load_library()
     if adv is None:
-        adv = torch.empty(R, dtype=torch.float32, device=dev)
+        adv = torch.empty(R, dtype=torch.float32)
     if ws is None:
         ws = alloc_workspace(advantage_workspace_size(R), dev)
     _check(lib.rlk_group_advantage(R, _ptr(rewards), _ptr(group_ids), adv_eps, _ptr(adv), _ptr(group_index),
@@ -250,6 +333,25 @@ def pg_loss_fwd_bwd(hidden, W, targets, mask, cu_seqlens, old_logp, rewards, gro
     replaces the group advantages (PPO)."""
     import torch
 
+    N, d, V, R, dev = _check_rows(hidden, W, targets, mask, cu_seqlens)
+    f32 = (torch.float32,)
+    _tensor(old_logp, "old_logp", shape=(N,), dtypes=f32)
+    _tensor(rewards, "rewards", shape=(R,), dtypes=f32)
+    _tensor(group_ids, "group_ids", shape=(R,), dtypes=(torch.int32,))
+    _tensor(loss, "loss", shape=(None,), dtypes=f32, optional=True, min_bytes=4)
+    _tensor(dhidden, "dhidden", shape=(N, d), dtypes=(hidden.dtype,), optional=True)
+    _tensor(dW, "dW", shape=(V, d), dtypes=f32, optional=True)
+    _tensor(logp_out, "logp_out", shape=(N,), dtypes=f32, optional=True)
+    _tensor(entropy_out, "entropy_out", shape=(N,), dtypes=f32, optional=True)
+    _tensor(stats, "stats", shape=(None,), dtypes=(torch.uint8,), optional=True,
+            min_bytes=ctypes.sizeof(PgStats))
+    _tensor(ws, "ws", dtypes=(torch.uint8,), optional=True)
+    for name, t in (("rollout_logp", rollout_logp), ("ref_logp", ref_logp), ("token_adv", token_adv)):
+        _tensor(t, name, shape=(N,), dtypes=f32, optional=True)
+    _on_one_gpu(hidden=hidden, W=W, targets=targets, mask=mask, cu_seqlens=cu_seqlens, old_logp=old_logp,
+                rewards=rewards, group_ids=group_ids, loss=loss, dhidden=dhidden, dW=dW, logp_out=logp_out,
+                entropy_out=entropy_out, stats=stats, ws=ws, rollout_logp=rollout_logp, ref_logp=ref_logp,
+                token_adv=token_adv)
     lib = load_library()
     if rollout_logp is not None or ref_logp is not None or token_adv is not None:
         params = PgParams.from_buffer_copy(bytes(params))
@@ -257,13 +359,12 @@ def pg_loss_fwd_bwd(hidden, W, targets, mask, cu_seqlens, old_logp, rewards, gro
         params.ref_logp = _ptr(ref_logp)
         params.token_adv = _ptr(token_adv)
     b = make_batch(hidden, W, cu_seqlens, temperature)
-    dev = hidden.device
     if loss is None:
-        loss = torch.empty(1, dtype=torch.float32, device=dev)
+        loss = torch.empty(1, dtype=torch.float32)
     if dhidden is None:
         dhidden = torch.empty_like(hidden)
     if dW is None:
-        dW = torch.empty(W.shape, dtype=torch.float32, device=dev)
+        dW = torch.empty(W.shape, dtype=torch.float32)
     if ws is None:
         ws = alloc_workspace(workspace_size(b, params), dev)
     _check(lib.rlk_pg_loss_fwd_bwd(ctypes.byref(b), _ptr(hidden), _ptr(W), _ptr(targets), _ptr(mask),
@@ -277,8 +378,20 @@ def gae(values, rewards, mask, cu_seqlens, group_ids=None, gamma=1.0, lam=1.0, a
     """Masked GAE per rollout (see rlk_gae); returns (adv, returns) as [N] fp32 device tensors."""
     import torch
 
+    f32 = (torch.float32,)
+    _tensor(values, "values", shape=(None,), dtypes=f32)
+    dev = values.device
+    N = values.shape[0]
+    _tensor(rewards, "rewards", shape=(None,), dtypes=f32)
+    R = rewards.shape[0]
+    _tensor(cu_seqlens, "cu_seqlens", shape=(R + 1,), dtypes=(torch.int32,))
+    _tensor(mask, "mask", shape=(N,), dtypes=(torch.uint8, torch.bool))
+    _tensor(group_ids, "group_ids", shape=(R,), dtypes=(torch.int32,), optional=True)
+    _tensor(adv, "adv", shape=(N,), dtypes=f32, optional=True)
+    _tensor(returns, "returns", shape=(N,), dtypes=f32, optional=True)
+    _on_one_gpu(values=values, rewards=rewards, cu_seqlens=cu_seqlens, mask=mask, group_ids=group_ids, adv=adv,
+                returns=returns)
     lib = load_library()
-    N, R = values.shape[0], rewards.shape[0]
     if adv is None:
         adv = torch.empty(N, dtype=torch.float32, device=values.device)
     if returns is None:
@@ -298,18 +411,44 @@ def value_loss(values, returns, mask, cu_seqlens, group_ids=None, loss=None, dva
     """Masked mean-squared value loss and its gradient (see rlk_value_loss)."""
     import torch
 
-    lib = load_library()
-    N, R = values.shape[0], cu_seqlens.shape[0] - 1
+    f32 = (torch.float32,)
+    _tensor(values, "values", shape=(None,), dtypes=f32)
     dev = values.device
+    N = values.shape[0]
+    _tensor(cu_seqlens, "cu_seqlens", shape=(None,), dtypes=(torch.int32,))
+    R = cu_seqlens.shape[0] - 1
+    _tensor(returns, "returns", shape=(N,), dtypes=f32)
+    _tensor(mask, "mask", shape=(N,), dtypes=(torch.uint8, torch.bool))
+    _tensor(group_ids, "group_ids", shape=(R,), dtypes=(torch.int32,), optional=True)
+    _tensor(loss, "loss", shape=(None,), dtypes=f32, optional=True, min_bytes=4)
+    _tensor(dvalues, "dvalues", shape=(N,), dtypes=f32, optional=True)
+    _tensor(ws, "ws", dtypes=(torch.uint8,), optional=True)
+    _on_one_gpu(values=values, returns=returns, cu_seqlens=cu_seqlens, mask=mask, group_ids=group_ids, loss=loss,
+                dvalues=dvalues, ws=ws)
+    lib = load_library()
     if loss is None:
-        loss = torch.empty(1, dtype=torch.float32, device=dev)
+        loss = torch.empty(1, dtype=torch.float32)
     if dvalues is None:
-        dvalues = torch.empty(N, dtype=torch.float32, device=dev)
+        dvalues = torch.empty(N, dtype=torch.float32)
     if ws is None:
         ws = alloc_workspace(value_workspace_size(R), dev)
     _check(lib.rlk_value_loss(N, R, _ptr(cu_seqlens), _ptr(mask), _ptr(values), _ptr(returns), _ptr(group_ids),
                               _ptr(loss), _ptr(dvalues), _ptr(ws), ws.numel(), _stream_handle(stream)))
     return loss, dvalues
+
+
+def _check_head(hidden, w_v, mask, cu_seqlens, group_ids):
+    import torch
+
+    _tensor(hidden, "hidden", shape=(None, None), dtypes=_float_types())
+    N, d = hidden.shape
+    dev = hidden.device
+    _tensor(w_v, "w_v", shape=(d,), dtypes=(hidden.dtype,))
+    _tensor(mask, "mask", shape=(N,), dtypes=(torch.uint8, torch.bool), optional=True)
+    _tensor(cu_seqlens, "cu_seqlens", shape=(None,), dtypes=(torch.int32,))
+    _tensor(group_ids, "group_ids", shape=(cu_seqlens.shape[0] - 1,), dtypes=(torch.int32,),
+            optional=True)
+    return N, d, dev
 
 
 def _head_batch(hidden, cu_seqlens) -> Batch:
@@ -321,6 +460,9 @@ def value_head_fwd(hidden, w_v, b_v, mask, cu_seqlens, group_ids=None, values=No
     """Linear value head values[t] = w_v . hidden[t] + b_v on the policy rows (see rlk_value_head_fwd)."""
     import torch
 
+    N, d, dev = _check_head(hidden, w_v, mask, cu_seqlens, group_ids)
+    _tensor(values, "values", shape=(N,), dtypes=(torch.float32,), optional=True)
+    _on_one_gpu(hidden=hidden, w_v=w_v, mask=mask, cu_seqlens=cu_seqlens, group_ids=group_ids, values=values)
     lib = load_library()
     b = _head_batch(hidden, cu_seqlens)
     if values is None:
@@ -342,13 +484,21 @@ def value_head_bwd(hidden, w_v, mask, cu_seqlens, group_ids, dvalues, dhidden=No
     """Backward of the linear value head (see rlk_value_head_bwd); returns (dhidden, dw_v, db_v)."""
     import torch
 
+    N, d, dev = _check_head(hidden, w_v, mask, cu_seqlens, group_ids)
+    f32 = (torch.float32,)
+    _tensor(dvalues, "dvalues", shape=(N,), dtypes=f32)
+    _tensor(dhidden, "dhidden", shape=(N, d), dtypes=(hidden.dtype,), optional=True)
+    _tensor(dw_v, "dw_v", shape=(d,), dtypes=f32, optional=True)
+    _tensor(db_v, "db_v", shape=(None,), dtypes=f32, optional=True, min_bytes=4)
+    _tensor(ws, "ws", dtypes=(torch.uint8,), optional=True)
+    _on_one_gpu(hidden=hidden, w_v=w_v, mask=mask, cu_seqlens=cu_seqlens, group_ids=group_ids, dvalues=dvalues,
+                dhidden=dhidden, dw_v=dw_v, db_v=db_v, ws=ws)
     lib = load_library()
     b = _head_batch(hidden, cu_seqlens)
-    dev = hidden.device
     if dw_v is None:
-        dw_v = torch.empty(hidden.shape[1], dtype=torch.float32, device=dev)
+        dw_v = torch.empty(hidden.shape[1], dtype=torch.float32)
     if db_v is None:
-        db_v = torch.empty(1, dtype=torch.float32, device=dev)
+        db_v = torch.empty(1, dtype=torch.float32)
     if ws is None:
         ws = alloc_workspace(value_head_workspace_size(hidden, cu_seqlens), dev)
     _check(lib.rlk_value_head_bwd(ctypes.byref(b), _ptr(hidden), _ptr(w_v), _ptr(mask), _ptr(group_ids),
@@ -428,7 +578,7 @@ def stats_from_tensor(t) -> dict:
 def stats_buffer(device="cuda"):
     import torch
 
-    return torch.zeros(ctypes.sizeof(PgStats), dtype=torch.uint8, device=device)
+    return torch.zeros(ctypes.sizeof(PgStats), dtype=torch.uint8ice)
 
 
 def profile_begin():

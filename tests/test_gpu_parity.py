@@ -9,7 +9,7 @@ that the oracle computes one by one and on properties that hold at any size.
 import numpy as np
 import pytest
 
-from gpu_common import (TOL_GRAD, TOL_LOSS, aux_logps, TOL_LOGP, O, WL, build_instance, compare_full, ensure_library, log,
+from gpu_common import (TOL_GRAD, TOL_LOSS, aux_logps, loss_error, TOL_LOGP, O, WL, build_instance, compare_full, ensure_library, log,
                         params_for, rel_fro, rlk, run_gpu, run_oracle, to_host)
 
 pytestmark = pytest.mark.gpu
@@ -344,7 +344,8 @@ def test_full_size_sampled_rows(name):
                                         entropy_coef=p.entropy_coef, agg=p.agg)
     s_tok, _, _ = O.surrogate(lp_all, old_pol, adv_tok, p.eps_low, p.eps_high)
     scale = float(np.abs(omega * (s_tok + p.entropy_coef * en_all)).sum())
-    e_loss = abs(gpu["loss"] - loss_ref) / max(scale, 1e-30)
+    e_loss_l1 = abs(gpu["loss"] - loss_ref) / max(scale, 1e-30)
+    e_loss = loss_error(gpu["loss"], loss_ref, scale)
 
     # dW rows: seeded vocabulary ids, a quarter of them targets of policy tokens (the one-hot term)
     rng = np.random.default_rng(cfg.seed + 11)
@@ -360,7 +361,7 @@ def test_full_size_sampled_rows(name):
     colsum = to_host(gpu["dW"].sum(dim=0))
     rel_cs = float(np.abs(colsum).max() / max(1e-30, float(gpu["dW"].abs().sum(dim=0).max())))
     log(f"  {N_SAMPLED_ROWS} sampled rows: logp {e_lp:.3g} ent {e_en:.3g} dh {e_dh:.3g}; loss {e_loss:.3g} "
-        f"(gpu {gpu['loss']:.6g} ref {loss_ref:.6g}); {v_sel.shape[0]} dW rows {e_dw:.3g}; dW colsum rel "
+        f"(gpu {gpu['loss']:.6g} ref {loss_ref:.6g}); {v_sel.shape[0]} dW rows {e_dw:.3g}; loss/L1 {e_loss_l1:.3g}; dW colsum rel "
         f"{rel_cs:.3g}; oracle {time.time() - t0:.1f} s")
     tol = TOL_LOGP[cfg.dtype]
     assert e_lp <= tol and e_en <= tol and e_dh <= TOL_GRAD
