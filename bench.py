@@ -71,9 +71,10 @@ def kernel_source_digest() -> str:
     return h.hexdigest()[:16]
 
 
-def read_traffic(kernel: str, workload: str, digest: str):
+def read_traffic(kernel: str, workload: str, digest: str, launches_per_step=None):
     """HBM bytes per launch of `kernel` from the committed rocprofv3 counter summary, if it was
-    taken from the current kernel sources (else None)."""
+    taken from the current kernel sources and (when given) with the same launches per step (else
+    None: a per-launch average over another chunk loop does not describe this run's launches)."""
     path = os.path.join(PROFILES, f"{kernel}_{workload}_traffic.txt")
     if not os.path.exists(path):
         return None
@@ -84,13 +85,26 @@ def read_traffic(kernel: str, workload: str, digest: str):
             kv[k.strip()] = v.strip()
     if kv.get("kernel_source_digest") != digest:
         return None
+    if launches_per_step is not None and kv.get("launches_per_step") != str(int(launches_per_step)):
+        return None
     try:
         return float(kv["hbm_bytes_per_launch"])
     except (KeyError, ValueError):
         return None
 
 
-def cpu_baseline(cfg, inp, target_tokens: int):
+def host_policy_tokens(st, exclusion: bool = True) -> int:
+    """Trained tokens of a batch counted on the host from its structure (mask = 1, in rollouts with a
+    group id >= 0 when `exclusion`): the bound a data pipeline that builds the masks knows before the
+    call.  The log-prob forward has no exclusion (exclusion=False)."""
+    import numpy as np
+
+    lens = np.diff(np.asarray(st.cu_seqlens, dtype=np.int64))
+    keep = np.repeat(np.asarray(st.group_ids) >= 0 if exclusion else np.ones(len(lens), bool), lens)
+    return int((np.asarray(st.mask)[:keep.shape[0]].astype(bool) & keep).sum())
+
+
+def cpu_baseline(cfg, inp, target_tokens: int, n_eff_full: int):
     """The fp64 oracle, as it stands, on the first rollouts of the same batch (>= target_tokens
     policy tokens): forward, loss terms, dhidden rows and their dW contribution."""
     import numpy as np
@@ -121,10 +135,25 @@ def cpu_baseline(cfg, inp, target_tokens: int):
                             eps_high=cfg.eps_high, entropy_coef=cfg.entropy_coef)
     dt = time.perf_counter() - t0
     ntok = out["stats"]["n_policy_tokens"]
+    affinity = sorted(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else []
     return {"value": ntok / dt, "unit": "policy tokens/s", "cores": threads or os.cpu_count(), "kind": "oracle",
             "sample": f"first {keep_rollouts} rollouts ({ntok} policy tokens, full V={cfg.V}, d={cfg.d}, "
                       f"fwd+loss+dhidden+dW contribution), fp64 NumPy, {dt:.1f} s",
-            "seconds": dt}
+            "seconds": dt, "blas_threads": threads, "os_cpu_count": os.cpu_count(),
+            "affinity_cores": len(affinity), "affinity": _ranges(affinity),
+            "full_config_s_extrapolated": n_eff_full * dt / max(1, ntok)}
+
+
+def _ranges(cpus):
+    """Compact text of a CPU list: 0-15,32-47."""
+    out, i = [], 0
+    while i < len(cpus):
+        j = i
+        while j + 1 < len(cpus) and cpus[j + 1] == cpus[j] + 1:
+            j += 1
+        out.append(str(cpus[i]) if i == j else f"{cpus[i]}-{cpus[j]}")
+        i = j + 1
+    return ",".join(out)
 
 
 COPY_TAG = "neg"   # the calibration copy is torch.neg on fp32 (reads and writes its size once)
@@ -202,10 +231,16 @@ def occupancy_summary(counter_csv, title, cmd):
     out = [f"# {title}", f"# command: {cmd}",
            "# summary: python bench.py --occupancy-summary <counter_collection.csv> (launches >= 1 ms)",
            f"# clock = GRBM_GUI_ACTIVE / {N_XCD} / time; occupancy = SQ_VALU_MFMA_BUSY_CYCLES / {N_SIMD} / "
-           f"(GRBM_GUI_ACTIVE / {N_XCD}); wait = SQ_WAIT_ANY / SQ_WAVE_CYCLES",
-           f"{'kernel':14s} {'launches':>8s} {'avg_ms':>8s} {'clock_GHz':>9s} {'mfma_occ':>8s} {'wait':>6s}"]
+           f"(GRBM_GUI_ACTIVE / {N_XCD}); wait = SQ_WAIT_ANY / SQ_WAVE_CYCLES; executed FLOP = "
+           f"SQ_INSTS_VALU_MFMA_MOPS_BF16 * 512 (all launches of the step)",
+           f"{'kernel':14s} {'launches':>8s} {'avg_ms':>8s} {'clock_GHz':>9s} {'mfma_occ':>8s} {'wait':>6s} "
+           f"{'exec_TFLOP':>10s}"]
+    total_flop = 0.0
     for kind in GEMM_KINDS:
-        runs = [d for d in per.get(kind, {}).values() if d["ns"] >= 1_000_000 and "GRBM_GUI_ACTIVE" in d]
+        allruns = list(per.get(kind, {}).values())
+        flop = sum(d.get("SQ_INSTS_VALU_MFMA_MOPS_BF16", 0.0) for d in allruns) * 512.0
+        total_flop += flop
+        runs = [d for d in allruns if d["ns"] >= 1_000_000 and "GRBM_GUI_ACTIVE" in d]
         if not runs:
             continue
         ns = sum(d["ns"] for d in runs)
@@ -213,8 +248,32 @@ def occupancy_summary(counter_csv, title, cmd):
         busy = sum(d["SQ_VALU_MFMA_BUSY_CYCLES"] for d in runs) / N_SIMD
         wait = sum(d["SQ_WAIT_ANY"] for d in runs) / max(1.0, sum(d["SQ_WAVE_CYCLES"] for d in runs))
         out.append(f"{kind:14s} {len(runs):8d} {ns / len(runs) / 1e6:8.2f} {cyc / ns:9.2f} {busy / cyc:8.3f} "
-                   f"{wait:6.3f}")
+                   f"{wait:6.3f} {flop / 1e12:10.2f}")
+    if total_flop > 0:
+        out.append(f"executed_mfma_flop_per_step: {total_flop:.6e}")
+    out.append(f"kernel_source_digest: {kernel_source_digest()}")
     return "\n".join(out) + "\n"
+
+
+def read_occupancy(workload: str, digest: str):
+    """(executed MFMA FLOP per step, {gemm: MFMA pipe occupancy}) from the committed counter summary of
+    this workload, if it was taken from the current GEMM sources (else None)."""
+    path = os.path.join(PROFILES, f"gemm_occupancy_{workload}.txt")
+    if not os.path.exists(path):
+        return None
+    flop, occ, dig = None, {}, None
+    for line in open(path):
+        if line.startswith("executed_mfma_flop_per_step:"):
+            flop = float(line.split(":", 1)[1])
+        elif line.startswith("kernel_source_digest:"):
+            dig = line.split(":", 1)[1].strip()
+        else:
+            f = line.split()
+            if len(f) >= 5 and f[0] in GEMM_KINDS:
+                occ[f[0]] = float(f[4])
+    if dig != digest or flop is None:
+        return None
+    return flop, occ
 
 
 HBM_KERNELS = ("k_dz", "k_gather", "k_transpose_w", "k_zero_fill", "k_combine")
@@ -411,6 +470,11 @@ def main():
     ap.add_argument("--graph", action="store_true",
                     help="capture one step as a HIP graph and replay it (launch-bound workloads); no per-kernel events")
     ap.add_argument("--cpu-tokens", type=int, default=1024)
+    ap.add_argument("--no-policy-bound", action="store_true",
+                    help="do not pass the host-known count of policy tokens (max_policy_tokens = 0: the chunk loop "
+                         "covers all N rows)")
+    ap.add_argument("--logprob-only", action="store_true",
+                    help="time rlk_logprob_fwd alone (the pi_old forward pass, 2 N_eff V d FLOP per call)")
     ap.add_argument("--no-kernel-events", action="store_true",
                     help="time the steps without per-kernel HIP events (roofline then null)")
     ap.add_argument("--calibrate-copy-mib", type=int, default=0,
@@ -472,20 +536,30 @@ def main():
     dev = "cuda"
     params = rlk.make_params(eps_low=cfg.eps_low, eps_high=cfg.eps_high, entropy_coef=cfg.entropy_coef,
                              chunk_rows=args.chunk_rows)
-    batch = rlk.make_batch(inp["h"], inp["W"], inp["cu"])
-    ws = rlk.alloc_workspace(rlk.workspace_size(batch, params), dev)
+    bound = 0 if args.no_policy_bound else host_policy_tokens(st, exclusion=not args.logprob_only)
+    batch = rlk.make_batch(inp["h"], inp["W"], inp["cu"], max_policy_tokens=bound)
+    ws = rlk.alloc_workspace(rlk.workspace_size(batch, None if args.logprob_only else params), dev)
     ws_adv = rlk.alloc_workspace(rlk.advantage_workspace_size(R), dev)
     adv = torch.empty(R, dtype=torch.float32, device=dev)
     loss = torch.empty(1, dtype=torch.float32, device=dev)
     dh = torch.empty_like(inp["h"])
     dW = torch.empty(inp["W"].shape, dtype=torch.float32, device=dev)
     stats = rlk.stats_buffer(dev)
+    logp = torch.empty(N, dtype=torch.float32, device=dev)
 
     def step():
         # both calls go to torch's current stream (the capture stream while a graph is recorded)
         rlk.group_advantage(inp["rewards"], inp["gid"], params.adv_eps, adv=adv, ws=ws_adv)
         rlk.pg_loss_fwd_bwd(inp["h"], inp["W"], inp["targets"], inp["mask"], inp["cu"], inp["old"], inp["rewards"],
-                            inp["gid"], params, loss=loss, dhidden=dh, dW=dW, stats=stats, ws=ws)
+                            inp["gid"], params, loss=loss, dhidden=dh, dW=dW, stats=stats, ws=ws,
+                            max_policy_tokens=bound)
+
+    def logprob_step():
+        rlk.logprob_fwd(inp["h"], inp["W"], inp["targets"], inp["mask"], inp["cu"], logp=logp, ws=ws,
+                        max_policy_tokens=bound)
+
+    if args.logprob_only:
+        step = logprob_step
 
     if args.calibrate_copy_mib > 0:
         n = args.calibrate_copy_mib * (1 << 20) // 4
@@ -501,8 +575,11 @@ def main():
     torch.cuda.synchronize()
     if rlk.check_status(ws) != 0:
         raise SystemExit("device data error in the benchmark batch")
-    s = rlk.stats_from_tensor(stats)
-    n_eff = int(s["n_policy_tokens"])
+    n_eff = host_policy_tokens(st, exclusion=not args.logprob_only)
+    if not args.logprob_only:
+        s = rlk.stats_from_tensor(stats)
+        if int(s["n_policy_tokens"]) != n_eff:
+            raise SystemExit(f"policy tokens: device {int(s['n_policy_tokens'])}, host {n_eff}")
 
     if args.next_rows:
         print(json.dumps(next_rows(cfg, inp, params, args.steps)), flush=True)
@@ -525,21 +602,29 @@ def main():
         log("[bench] step captured as a graph")
     log(f"[bench] timing {args.steps} step(s)")
     use_events = not args.no_kernel_events and not args.graph
+    # per-step events on the stream the library launches on (torch's current stream)
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
     torch.cuda.synchronize()
     if use_events:
-        rlk.profile_begin()
+        rlk.profile_begin()   # creates its event pool here, outside the timed region
+    torch.cuda.synchronize()
     t0 = time.perf_counter()
-    for _ in range(args.steps):
+    ev[0].record()
+    for i in range(args.steps):
         run()
+        ev[i + 1].record()
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     kern = rlk.profile_end() if use_events else {}
-    ms_per_step = (t1 - t0) * 1e3 / args.steps
+    step_ms = [ev[i].elapsed_time(ev[i + 1]) for i in range(args.steps)]
+    ms_per_step = float(np.median(step_ms))
     value = n_eff / (ms_per_step / 1e3)
-    alg_flops = 6.0 * n_eff * cfg.V * cfg.d
+    n_mm = 1 if args.logprob_only else 3
+    alg_flops = 2.0 * n_mm * n_eff * cfg.V * cfg.d
     peak = PEAK_BF16 if cfg.dtype == "bf16" else PEAK_FP32_MFMA
     mfma_frac = alg_flops / (ms_per_step / 1e3) / peak
-    log(f"[bench] {ms_per_step:.2f} ms/step, {value:.0f} policy tokens/s, {100 * mfma_frac:.1f}% of MFMA peak")
+    log(f"[bench] {ms_per_step:.2f} ms/step (median; mean {np.mean(step_ms):.2f}, wall {(t1 - t0) * 1e3 / args.steps:.2f}), "
+        f"{value:.0f} policy tokens/s, {100 * mfma_frac:.1f}% of MFMA peak")
 
     roofline = None
     per_kernel = {}
@@ -552,26 +637,40 @@ def main():
         flops_per_launch = 2.0 * n_eff * cfg.V * cfg.d * args.steps / cnt
         achieved = flops_per_launch / (avg_ms / 1e3) / 1e12
         digest = kernel_source_digest()
-        traffic = read_traffic(dom, cfg.name, digest)
+        traffic = None if args.logprob_only else read_traffic(dom, cfg.name, digest, cnt // args.steps)
         roofline = {"kernel": dom, "bound": "mfma", "achieved": round(achieved, 1), "peak": peak / 1e12,
                     "unit": "TFLOP/s", "frac": round(achieved * 1e12 / peak, 4), "traffic": traffic,
                     "avg_launch_ms": round(avg_ms, 3), "launches": cnt,
                     "flops_per_launch": flops_per_launch, "kernel_source_digest": digest}
         log("[bench] per-kernel ms/step: " + ", ".join(f"{k}={v['ms_per_step']}" for k, v in per_kernel.items()))
 
+    executed = None
+    occ = None if (args.logprob_only or args.graph or args.group_share > 1) else read_occupancy(cfg.name, kernel_source_digest())
+    if occ is not None:
+        flop, pipe = occ
+        executed = {"mfma_flop_per_step": flop, "pct_of_peak": round(100 * flop / (ms_per_step / 1e3) / peak, 2),
+                    "mfma_pipe_busy": pipe, "source": f"profiles/gemm_occupancy_{cfg.name}.txt"}
+
     cpu = None
     if not args.no_cpu_baseline:
         log(f"[bench] timing the fp64 oracle on >= {args.cpu_tokens} policy tokens")
-        cpu = cpu_baseline(cfg, inp, args.cpu_tokens)
+        cpu = cpu_baseline(cfg, inp, args.cpu_tokens, n_eff)
         log(f"[bench] oracle {cpu['value']:.1f} policy tokens/s in {cpu['seconds']:.1f} s")
 
+    metric = METRIC if not args.logprob_only else "policy tokens/sec for the logprob forward (pi_old pass); % of bf16 MFMA peak"
     out = {
-        "metric": METRIC, "value": round(value, 1), "unit": "policy tokens/s", "n_gpus": 1, "steps": args.steps,
+        "metric": metric, "value": round(value, 1), "unit": "policy tokens/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": round(ms_per_step, 3), "higher_is_better": True, "scaling": "weak",
         "vs_baseline": None, "dtype": cfg.dtype, "data": "synthetic",
         "config": dict(WL.configs.describe(cfg, N), N_eff=n_eff, chunk_rows=args.chunk_rows or "auto",
-                       **({"graph": True} if args.graph else {})),
+                       max_policy_tokens=bound, **({"graph": True} if args.graph else {}),
+                       **({"call": "rlk_logprob_fwd"} if args.logprob_only else {})),
+        "timing": {"ms_per_step_median": round(ms_per_step, 3), "ms_per_step_mean": round(float(np.mean(step_ms)), 3),
+                   "ms_per_step_min": round(float(np.min(step_ms)), 3), "ms_per_step_max": round(float(np.max(step_ms)), 3),
+                   "ms_wall_per_step": round((t1 - t0) * 1e3 / args.steps, 3),
+                   "per_kernel_events": use_events},
         "mfma_pct_of_peak": round(100 * mfma_frac, 2),
+        "executed_mfma_pct": executed["pct_of_peak"] if executed else None, "executed_mfma": executed,
         "roofline": roofline, "cpu_baseline": cpu, "kernels": per_kernel,
     }
     print(json.dumps(out), flush=True)

@@ -48,7 +48,7 @@
 extern "C" {
 #endif
 
-#define RLK_VERSION 4
+#define RLK_VERSION 5
 
 typedef int32_t rlk_status_t;
 enum {
@@ -72,8 +72,10 @@ enum { RLK_AGG_SEQ_MEAN_TOKEN_MEAN = 0, RLK_AGG_TOKEN_MEAN = 1 };
 
 /* Bits of the device status word (rlk_check_status). */
 enum {
-  RLK_DERR_TARGET = 1,     /* a policy row's target lies outside [0, V) */
-  RLK_DERR_CU_SEQLENS = 2  /* cu[0] != 0, cu decreasing, or cu[R] != N */
+  RLK_DERR_TARGET = 1,       /* a policy row's target lies outside [0, V) */
+  RLK_DERR_CU_SEQLENS = 2,   /* cu[0] != 0, cu decreasing, or cu[R] != N */
+  RLK_DERR_POLICY_BOUND = 4  /* more trained tokens than rlk_batch_t.max_policy_tokens; the
+                                outputs of that call are not valid */
 };
 
 /* Size limits: the GEMMs address 256-row operand panels with 32-bit buffer offsets, so a
@@ -90,7 +92,12 @@ typedef struct {
   const int32_t* cu_seqlens;  /* device [R+1] */
   float temperature;          /* sampling temperature tau of the policy: logits z = W h / tau;
                                  0 means 1 (the default); otherwise finite and > 0 */
-  int32_t reserved;           /* must be 0 */
+  int32_t max_policy_tokens;  /* optional host-known upper bound on the trained tokens (mask = 1 in
+                                 non-excluded rollouts): 0 = unknown, the chunk loop then covers all
+                                 N rows and skips empty chunks on the device; > 0 sizes the chunk
+                                 loop for at most that many tokens (fewer launches, chunk rows
+                                 chosen for whole waves of GEMM tiles).  A batch holding more sets
+                                 RLK_DERR_POLICY_BOUND.  Must be >= 0. */
 } rlk_batch_t;
 
 typedef struct {
@@ -291,8 +298,10 @@ int32_t rlk_version(void);
 
 /* Kernel timing for measurement.  Between rlk_profile_begin() and rlk_profile_end() every
  * kernel launch of the entry points above is bracketed by a pair of HIP events on the
- * call's stream.  rlk_profile_end() waits for them and fills, per kernel kind k < *n_kinds
- * (host arrays of length max_kinds), the summed milliseconds and the launch count. */
+ * call's stream.  rlk_profile_begin() creates the events beforehand (a pool of 8192, reused by
+ * later windows; more are created only if a window records more), so the launches inside the
+ * window allocate nothing.  rlk_profile_end() waits for them and fills, per kernel kind
+ * k < *n_kinds (host arrays of length max_kinds), the summed milliseconds and the launch count. */
 rlk_status_t rlk_profile_begin(void);
 rlk_status_t rlk_profile_end(int32_t max_kinds, double* total_ms, int32_t* launches,
                              int32_t* n_kinds);

@@ -17,7 +17,7 @@ LIB_PATH = os.path.join(PKG_DIR, "librlk.so")
 RLK_OK, RLK_EINVAL, RLK_ESHAPE, RLK_EDTYPE, RLK_EWORKSPACE, RLK_EHIP, RLK_EDATA = range(7)
 DTYPE_F32, DTYPE_BF16 = 0, 1
 AGG_SEQ, AGG_TOKEN = 0, 1
-DERR_TARGET, DERR_CU_SEQLENS = 1, 2
+DERR_TARGET, DERR_CU_SEQLENS, DERR_POLICY_BOUND = 1, 2, 4
 
 EXPORTS = [
     "rlk_workspace_size", "rlk_advantage_workspace_size", "rlk_compact", "rlk_logprob_fwd", "rlk_group_advantage",
@@ -30,7 +30,7 @@ EXPORTS = [
 class Batch(ctypes.Structure):
     _fields_ = [("N", ctypes.c_int64), ("R", ctypes.c_int32), ("d", ctypes.c_int32), ("V", ctypes.c_int32),
                 ("dtype", ctypes.c_int32), ("cu_seqlens", ctypes.c_void_p), ("temperature", ctypes.c_float),
-                ("reserved", ctypes.c_int32)]
+                ("max_policy_tokens", ctypes.c_int32)]
 
 
 class PgParams(ctypes.Structure):
@@ -199,11 +199,14 @@ def _dtype_code(t) -> int:
     raise TypeError(f"unsupported dtype {t.dtype}")
 
 
-def make_batch(hidden, W, cu_seqlens, temperature: float = 1.0) -> Batch:
+def make_batch(hidden, W, cu_seqlens, temperature: float = 1.0, max_policy_tokens: int = 0) -> Batch:
+    """Batch descriptor; max_policy_tokens is an optional host-known upper bound on the trained
+    tokens (0 = unknown), see rlk_batch_t."""
     N, d = hidden.shape
     V = W.shape[0]
     R = cu_seqlens.shape[0] - 1
-    return Batch(N=N, R=R, d=d, V=V, dtype=_dtype_code(W), cu_seqlens=_ptr(cu_seqlens), temperature=temperature)
+    return Batch(N=N, R=R, d=d, V=V, dtype=_dtype_code(W), cu_seqlens=_ptr(cu_seqlens), temperature=temperature,
+                 max_policy_tokens=int(max_policy_tokens))
 
 
 def make_params(eps_low=0.2, eps_high=None, adv_eps=1e-6, entropy_coef=0.0, agg=AGG_SEQ, accumulate_dW=False,
@@ -243,14 +246,15 @@ def alloc_workspace(nbytes: int, device="cuda"):
     """A 256-byte aligned uint8 device buffer of at least nbytes (torch allocations are)."""
     import torch
 
-    ws = torch.empty(max(int(nbytes), 256), dtype=torch.uint8ice)
+    ws = torch.empty(max(int(nbytes), 256), dtype=torch.uint8, device=device)
     assert ws.data_ptr() % 256 == 0
     return ws
 
 
 def logprob_fwd(hidden, W, targets, mask, cu_seqlens, logp=None, entropy=None, lse=None, ws=None, stream=None,
-                temperature: float = 1.0):
-    """Per-token log-prob / entropy / log-partition of the sampled tokens (rows with mask 0 -> 0)."""
+                temperature: float = 1.0, max_policy_tokens: int = 0):
+    """Per-token log-prob / entropy / log-partition of the sampled tokens (rows with mask 0 -> 0).
+    max_policy_tokens: optional host-known bound on the policy tokens (rlk_batch_t)."""
     import torch
 
     N, d, V, R, dev = _check_rows(hidden, W, targets, mask, cu_seqlens)
@@ -262,11 +266,13 @@ def logprob_fwd(hidden, W, targets, mask, cu_seqlens, logp=None, entropy=None, l
     _on_one_gpu(hidden=hidden, W=W, targets=targets, mask=mask, cu_seqlens=cu_seqlens, logp=logp, entropy=entropy,
                 lse=lse, ws=ws)
     lib = load_library()
-    b = make_batch(hidden, W, cu_seqlens, temperature)
+    b = make_batch(hidden, W, cu_seqlens, temperature, max_policy_tokens)
     if logp is None:
-        logp = torch.empty(N, dtype=torch.float32)
+        logp = torch.empty(N, dtype=torch.float32, device=dev)
     if ws is None:
         ws = alloc_workspace(workspace_size(b), dev)
+    _on_one_gpu(hidden=hidden, W=W, targets=targets, mask=mask, cu_seqlens=cu_seqlens, logp=logp, entropy=entropy,
+                lse=lse, ws=ws)
     _check(lib.rlk_logprob_fwd(ctypes.byref(b), _ptr(hidden), _ptr(W), _ptr(targets), _ptr(mask), _ptr(logp),
                                _ptr(entropy), _ptr(lse), _ptr(ws), ws.numel(), _stream_handle(stream)))
     return logp, entropy, lse, ws
@@ -290,12 +296,14 @@ def compact(cu_seqlens, mask, group_ids=None, targets=None, N=None, V=1, d=8, ws
     _on_one_gpu(cu_seqlens=cu_seqlens, mask=mask, group_ids=group_ids, targets=targets, ws=ws)
     lib = load_library()
     b = Batch(N=N, R=R, d=d, V=V, dtype=DTYPE_BF16, cu_seqlens=_ptr(cu_seqlens))
-    idx = torch.empty(max(N, 1), dtype=torch.int32)
-    tokr = torch.empty(max(N, 1), dtype=torch.int32)
-    n_pol = torch.empty(max(R, 1), dtype=torch.int32)
-    n_eff = torch.empty(1, dtype=torch.int32)
+    idx = torch.empty(max(N, 1), dtype=torch.int32, device=dev)
+    tokr = torch.empty(max(N, 1), dtype=torch.int32, device=dev)
+    n_pol = torch.empty(max(R, 1), dtype=torch.int32, device=dev)
+    n_eff = torch.empty(1, dtype=torch.int32, device=dev)
     if ws is None:
         ws = alloc_workspace(workspace_size(b), dev)
+    _on_one_gpu(cu_seqlens=cu_seqlens, mask=mask, group_ids=group_ids, targets=targets, idx=idx, tokr=tokr,
+                n_pol=n_pol, n_eff=n_eff, ws=ws)
     _check(lib.rlk_compact(ctypes.byref(b), _ptr(mask), _ptr(group_ids), _ptr(targets), _ptr(idx), _ptr(tokr),
                            _ptr(n_pol), _ptr(n_eff), _ptr(ws), ws.numel(), _stream_handle(stream)))
     return idx, tokr, n_pol[:R], n_eff, ws
@@ -316,9 +324,10 @@ def group_advantage(rewards, group_ids, adv_eps=1e-6, adv=None, group_index=None
     _on_one_gpu(rewards=rewards, group_ids=group_ids, adv=adv, group_index=group_index, n_groups=n_groups, ws=ws)
     lib = load_library()
     if adv is None:
-        adv = torch.empty(R, dtype=torch.float32)
+        adv = torch.empty(R, dtype=torch.float32, device=dev)
     if ws is None:
         ws = alloc_workspace(advantage_workspace_size(R), dev)
+    _on_one_gpu(rewards=rewards, group_ids=group_ids, adv=adv, group_index=group_index, n_groups=n_groups, ws=ws)
     _check(lib.rlk_group_advantage(R, _ptr(rewards), _ptr(group_ids), adv_eps, _ptr(adv), _ptr(group_index),
                                    _ptr(n_groups), _ptr(ws), ws.numel(), _stream_handle(stream)))
     return adv
@@ -326,11 +335,13 @@ def group_advantage(rewards, group_ids, adv_eps=1e-6, adv=None, group_index=None
 
 def pg_loss_fwd_bwd(hidden, W, targets, mask, cu_seqlens, old_logp, rewards, group_ids, params: PgParams,
                     loss=None, dhidden=None, dW=None, logp_out=None, entropy_out=None, stats=None, ws=None,
-                    stream=None, rollout_logp=None, ref_logp=None, token_adv=None, temperature: float = 1.0):
+                    stream=None, rollout_logp=None, ref_logp=None, token_adv=None, temperature: float = 1.0,
+                    max_policy_tokens: int = 0):
     """Loss, dL/dhidden and dL/dW of the masked clipped policy-gradient objective.
     rollout_logp / ref_logp ([N] fp32 device tensors or None) feed truncated importance sampling
     (params.tis_cap) and the KL term (params.kl_coef); token_adv ([N] fp32, e.g. from gae())
-    replaces the group advantages (PPO)."""
+    replaces the group advantages (PPO); max_policy_tokens is an optional host-known bound on the
+    trained tokens that sizes the chunk loop (rlk_batch_t; the workspace must be sized with it)."""
     import torch
 
     N, d, V, R, dev = _check_rows(hidden, W, targets, mask, cu_seqlens)
@@ -358,15 +369,16 @@ def pg_loss_fwd_bwd(hidden, W, targets, mask, cu_seqlens, old_logp, rewards, gro
         params.rollout_logp = _ptr(rollout_logp)
         params.ref_logp = _ptr(ref_logp)
         params.token_adv = _ptr(token_adv)
-    b = make_batch(hidden, W, cu_seqlens, temperature)
+    b = make_batch(hidden, W, cu_seqlens, temperature, max_policy_tokens)
     if loss is None:
-        loss = torch.empty(1, dtype=torch.float32)
+        loss = torch.empty(1, dtype=torch.float32, device=dev)
     if dhidden is None:
         dhidden = torch.empty_like(hidden)
     if dW is None:
-        dW = torch.empty(W.shape, dtype=torch.float32)
+        dW = torch.empty(W.shape, dtype=torch.float32, device=dev)
     if ws is None:
         ws = alloc_workspace(workspace_size(b, params), dev)
+    _on_one_gpu(hidden=hidden, loss=loss, dhidden=dhidden, dW=dW, ws=ws)
     _check(lib.rlk_pg_loss_fwd_bwd(ctypes.byref(b), _ptr(hidden), _ptr(W), _ptr(targets), _ptr(mask),
                                    _ptr(old_logp), _ptr(rewards), _ptr(group_ids), ctypes.byref(params), _ptr(loss),
                                    _ptr(dhidden), _ptr(dW), _ptr(logp_out), _ptr(entropy_out), _ptr(stats),
@@ -396,6 +408,7 @@ def gae(values, rewards, mask, cu_seqlens, group_ids=None, gamma=1.0, lam=1.0, a
         adv = torch.empty(N, dtype=torch.float32, device=values.device)
     if returns is None:
         returns = torch.empty(N, dtype=torch.float32, device=values.device)
+    _on_one_gpu(values=values, adv=adv, returns=returns)
     _check(lib.rlk_gae(N, R, _ptr(cu_seqlens), _ptr(mask), _ptr(values), _ptr(rewards), _ptr(group_ids),
                        gamma, lam, _ptr(adv), _ptr(returns), _stream_handle(stream)))
     return adv, returns
@@ -427,11 +440,12 @@ def value_loss(values, returns, mask, cu_seqlens, group_ids=None, loss=None, dva
                 dvalues=dvalues, ws=ws)
     lib = load_library()
     if loss is None:
-        loss = torch.empty(1, dtype=torch.float32)
+        loss = torch.empty(1, dtype=torch.float32, device=dev)
     if dvalues is None:
-        dvalues = torch.empty(N, dtype=torch.float32)
+        dvalues = torch.empty(N, dtype=torch.float32, device=dev)
     if ws is None:
         ws = alloc_workspace(value_workspace_size(R), dev)
+    _on_one_gpu(values=values, loss=loss, dvalues=dvalues, ws=ws)
     _check(lib.rlk_value_loss(N, R, _ptr(cu_seqlens), _ptr(mask), _ptr(values), _ptr(returns), _ptr(group_ids),
                               _ptr(loss), _ptr(dvalues), _ptr(ws), ws.numel(), _stream_handle(stream)))
     return loss, dvalues
@@ -467,6 +481,7 @@ def value_head_fwd(hidden, w_v, b_v, mask, cu_seqlens, group_ids=None, values=No
     b = _head_batch(hidden, cu_seqlens)
     if values is None:
         values = torch.empty(hidden.shape[0], dtype=torch.float32, device=hidden.device)
+    _on_one_gpu(hidden=hidden, values=values)
     _check(lib.rlk_value_head_fwd(ctypes.byref(b), _ptr(hidden), _ptr(w_v), ctypes.c_float(b_v), _ptr(mask),
                                   _ptr(group_ids), _ptr(values), _stream_handle(stream)))
     return values
@@ -496,11 +511,12 @@ def value_head_bwd(hidden, w_v, mask, cu_seqlens, group_ids, dvalues, dhidden=No
     lib = load_library()
     b = _head_batch(hidden, cu_seqlens)
     if dw_v is None:
-        dw_v = torch.empty(hidden.shape[1], dtype=torch.float32)
+        dw_v = torch.empty(hidden.shape[1], dtype=torch.float32, device=dev)
     if db_v is None:
-        db_v = torch.empty(1, dtype=torch.float32)
+        db_v = torch.empty(1, dtype=torch.float32, device=dev)
     if ws is None:
         ws = alloc_workspace(value_head_workspace_size(hidden, cu_seqlens), dev)
+    _on_one_gpu(hidden=hidden, dhidden=dhidden, dw_v=dw_v, db_v=db_v, ws=ws)
     _check(lib.rlk_value_head_bwd(ctypes.byref(b), _ptr(hidden), _ptr(w_v), _ptr(mask), _ptr(group_ids),
                                   _ptr(dvalues), _ptr(dhidden), 1 if accumulate else 0, _ptr(dw_v), _ptr(db_v),
                                   _ptr(ws), ws.numel(), _stream_handle(stream)))
@@ -578,7 +594,7 @@ def stats_from_tensor(t) -> dict:
 def stats_buffer(device="cuda"):
     import torch
 
-    return torch.zeros(ctypes.sizeof(PgStats), dtype=torch.uint8ice)
+    return torch.zeros(ctypes.sizeof(PgStats), dtype=torch.uint8, device=device)
 
 
 def profile_begin():

@@ -100,7 +100,11 @@ k_count(const uint8_t* mask, const int32_t* cu, const int32_t* gid, int R, int64
   }
 }
 
-__global__ void __launch_bounds__(1024) k_scan(const int32_t* blkcnt, int32_t* blkoff, int nblk, WsHeader* hdr) {
+// Exclusive scan of the per-block counts; n_eff = the total.  With a caller bound on the trained
+// tokens (max_policy > 0) a larger total is flagged and n_eff clamped to the bound, so every later
+// kernel stays within the chunk loop the host sized for it.
+__global__ void __launch_bounds__(1024) k_scan(const int32_t* blkcnt, int32_t* blkoff, int nblk, int32_t max_policy,
+                                               WsHeader* hdr) {
   __shared__ int wsum[16];
   __shared__ int carry_s;
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
@@ -120,7 +124,14 @@ __global__ void __launch_bounds__(1024) k_scan(const int32_t* blkcnt, int32_t* b
     if (threadIdx.x == 1023) carry_s = carry + woff + inc;
     __syncthreads();
   }
-  if (threadIdx.x == 0) hdr->n_eff = carry_s;
+  if (threadIdx.x == 0) {
+    int n = carry_s;
+    if (max_policy > 0 && n > max_policy) {
+      atomicOr(&hdr->status, RLK_DERR_POLICY_BOUND);
+      n = max_policy;
+    }
+    hdr->n_eff = n;
+  }
 }
 
 __global__ void __launch_bounds__(kThreads)
@@ -298,7 +309,8 @@ hipError_t launch_begin(int32_t* status_hdr, const int32_t* cu, int R, int64_t N
 }
 
 hipError_t launch_compact(const uint8_t* mask, const int32_t* cu, const int32_t* gid, int R, int64_t N,
-                          const int32_t* targets, int V, char* ws, const WsLayout& L, hipStream_t s) {
+                          const int32_t* targets, int V, int32_t max_policy, char* ws, const WsLayout& L,
+                          hipStream_t s) {
   WsHeader* hdr = reinterpret_cast<WsHeader*>(ws + L.hdr);
   uint8_t* keep = reinterpret_cast<uint8_t*>(ws + L.keep);
   int32_t* blkcnt = reinterpret_cast<int32_t*>(ws + L.blkcnt);
@@ -308,7 +320,7 @@ hipError_t launch_compact(const uint8_t* mask, const int32_t* cu, const int32_t*
     k_count<<<L.nblk, kThreads, 0, s>>>(mask, cu, gid, R, N, keep, blkcnt);
     prof_mark(KK_COUNT, false, s);
     prof_mark(KK_SCAN, true, s);
-    k_scan<<<1, 1024, 0, s>>>(blkcnt, blkoff, L.nblk, hdr);
+    k_scan<<<1, 1024, 0, s>>>(blkcnt, blkoff, L.nblk, max_policy, hdr);
     prof_mark(KK_SCAN, false, s);
     prof_mark(KK_WRITE_IDX, true, s);
     k_write_idx<<<L.nblk, kThreads, 0, s>>>(keep, cu, R, N, blkoff, targets, V,

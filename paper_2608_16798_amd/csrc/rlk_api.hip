@@ -46,14 +46,14 @@ rlk_status_t report_error(rlk_status_t code, const char* msg) { return fail(code
 
 namespace {
 
-inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+constexpr size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 // Row tensors (hidden, W, dhidden) are read and written with 16-byte vector accesses.
 inline bool misaligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) != 0; }
 inline int64_t roundup(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
 
 struct Alloc {
   size_t off = 0;
-  size_t take(size_t bytes) {
+  constexpr size_t take(size_t bytes) {
     size_t o = off;
     off = align256(off + bytes);
     return o;
@@ -81,7 +81,7 @@ rlk_status_t check_batch(const rlk_batch_t* b) {
   if (b->R > 0 && !b->cu_seqlens) return fail(RLK_EINVAL, "cu_seqlens is NULL");
   if (b->temperature != 0.0f && !(b->temperature > 0.0f && isfinite(b->temperature)))
     return fail(RLK_EINVAL, "temperature must be 0 (= 1) or finite and > 0");
-  if (b->reserved != 0) return fail(RLK_EINVAL, "reserved must be 0");
+  if (b->max_policy_tokens < 0) return fail(RLK_EINVAL, "max_policy_tokens must be >= 0");
   return RLK_OK;
 }
 
@@ -109,6 +109,32 @@ void set_split(GemmArgs& g, const SplitK& p, char* part) {
 // 1 / tau of the batch's logits (z = W h / tau)
 float inv_temperature(const rlk_batch_t* b) { return b->temperature == 0.0f ? 1.0f : 1.0f / b->temperature; }
 
+// Rows per chunk for a batch known to hold at most B trained tokens, with at most cap rows per chunk:
+// the fewest chunks, and among the row counts giving that many, the one whose chunks fill the most
+// whole waves of 256 output tiles in the forward and dhidden GEMMs (the dW GEMM's tile count does
+// not depend on the chunk rows); ties go to the smaller workspace.
+int64_t plan_chunk_rows(int64_t B, int64_t cap, int64_t d, int64_t Vp) {
+  const int64_t nch = (B + cap - 1) / cap;
+  const int64_t rmin = roundup((B + nch - 1) / nch, kChunkAlign);
+  const int64_t tv = Vp / kTile, td = (d + kTile - 1) / kTile;
+  auto waves = [](int64_t tiles) { return (tiles + 255) / 256; };
+  int64_t best = rmin, best_cost = -1;
+  for (int64_t r = rmin; r <= cap; r += kChunkAlign) {
+    int64_t cost = 0, left = B;
+    for (int64_t c = 0; c < nch && left > 0; ++c) {
+      const int64_t rows = std::min(r, left), tc = (rows + kTile - 1) / kTile;
+      cost += waves(tv * tc) * d + waves(tc * td) * Vp;
+      left -= rows;
+    }
+    if (left > 0) continue;  // r too small for nch chunks
+    if (best_cost < 0 || cost < best_cost) {
+      best = r;
+      best_cost = cost;
+    }
+  }
+  return best;
+}
+
 rlk_status_t layout(const rlk_batch_t* b, bool bwd, int64_t chunk_rows, WsLayout& L) {
   const int64_t esz = b->dtype == RLK_DTYPE_BF16 ? 2 : 4;
   const int64_t N = b->N, R = b->R, d = b->d, V = b->V;
@@ -130,8 +156,11 @@ rlk_status_t layout(const rlk_batch_t* b, bool bwd, int64_t chunk_rows, WsLayout
     const int64_t cap = roundup(N > 0 ? N : 1, kChunkAlign);
     if (Mc > cap) Mc = cap;
   }
+  // rows the chunk loop has to cover: all N, or the caller's bound on the trained tokens
+  const int64_t B = b->max_policy_tokens > 0 ? std::min<int64_t>(b->max_policy_tokens, N) : N;
+  if (b->max_policy_tokens > 0 && B > 0) Mc = plan_chunk_rows(B, Mc, d, L.Vp);
   L.Mc = Mc;
-  L.nchunks = (int32_t)((N + Mc - 1) / Mc);
+  L.nchunks = (int32_t)((B + Mc - 1) / Mc);
   if (bwd && L.nchunks < 1) L.nchunks = 1;
 
   Alloc a;
@@ -180,7 +209,7 @@ rlk_status_t layout(const rlk_batch_t* b, bool bwd, int64_t chunk_rows, WsLayout
   return RLK_OK;
 }
 
-size_t advantage_ws_bytes(int32_t R) {
+constexpr size_t advantage_ws_bytes(int32_t R) {
   Alloc a;
   a.take(sizeof(WsHeader));
   a.take((size_t)R * 4);  // first
@@ -224,13 +253,26 @@ struct ProfRec {
   int kind;
   hipEvent_t a, b;
 };
+// Events are created when profiling begins (a pool reused across profiling windows), so a launch
+// inside the window only records two events and takes no allocation.
 struct Prof {
   std::mutex mu;
   bool on = false;
   std::vector<ProfRec> recs;
+  std::vector<hipEvent_t> pool;  // created events
+  size_t next = 0;               // first pool event not recorded in this window
   hipEvent_t open = nullptr;
   int open_kind = -1;
+  hipEvent_t take() {
+    if (next == pool.size()) {
+      hipEvent_t ev;
+      if (hipEventCreate(&ev) != hipSuccess) return nullptr;
+      pool.push_back(ev);
+    }
+    return pool[next++];
+  }
 };
+constexpr size_t kProfPoolEvents = 8192;
 Prof& prof() {
   static Prof p;
   return p;
@@ -248,20 +290,55 @@ void prof_mark(int kind, bool begin, hipStream_t s) {
   Prof& P = prof();
   if (!P.on) return;
   std::lock_guard<std::mutex> lk(P.mu);
-  hipEvent_t ev;
-  if (hipEventCreate(&ev) != hipSuccess) return;
-  (void)hipEventRecord(ev, s);
   if (begin) {
+    hipEvent_t ev = P.take();
+    if (!ev) return;
+    (void)hipEventRecord(ev, s);
     P.open = ev;
     P.open_kind = kind;
   } else if (P.open && P.open_kind == kind) {
+    hipEvent_t ev = P.take();
+    if (!ev) return;
+    (void)hipEventRecord(ev, s);
     P.recs.push_back({kind, P.open, ev});
     P.open = nullptr;
     P.open_kind = -1;
-  } else {
-    (void)hipEventDestroy(ev);
   }
 }
+
+namespace {
+
+rlk_status_t check_advantage_args(int32_t R, const float* rewards, const int32_t* group_ids, float adv_eps,
+                                  const float* adv) {
+  if (R < 0 || R > kMaxRollouts) return fail(RLK_ESHAPE, "R = %d outside [0, %d]", R, kMaxRollouts);
+  if (R > 0 && (!rewards || !group_ids || !adv)) return fail(RLK_EINVAL, "rewards, group_ids or adv is NULL");
+  if (!(adv_eps >= 0.0f) || !isfinite(adv_eps)) return fail(RLK_EINVAL, "adv_eps must be finite and >= 0");
+  return RLK_OK;
+}
+
+// The launches of rlk_group_advantage on a validated workspace of advantage_ws_bytes(R) bytes.
+rlk_status_t advantage_call(int32_t R, const float* rewards, const int32_t* group_ids, float adv_eps, float* adv,
+                            int32_t* group_index, int32_t* n_groups, void* ws, void* stream) {
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  Alloc a;
+  char* w = static_cast<char*>(ws);
+  WsHeader* hdr = reinterpret_cast<WsHeader*>(w + a.take(sizeof(WsHeader)));
+  int32_t* first = reinterpret_cast<int32_t*>(w + a.take((size_t)R * 4));
+  int32_t* gidx_ws = reinterpret_cast<int32_t*>(w + a.take((size_t)R * 4));
+  int32_t* gsize = reinterpret_cast<int32_t*>(w + a.take((size_t)R * 4));
+  double* gmu = reinterpret_cast<double*>(w + a.take((size_t)R * 8));
+  double* gsig = reinterpret_cast<double*>(w + a.take((size_t)R * 8));
+  int32_t* geq = reinterpret_cast<int32_t*>(w + a.take((size_t)R * 4));
+  int32_t* gidx = group_index ? group_index : gidx_ws;
+  RLK_TRY(launch_begin(reinterpret_cast<int32_t*>(hdr), nullptr, 0, 0, s), "begin");
+  RLK_TRY(launch_advantage(R, rewards, group_ids, adv_eps, first, gidx, gsize, gmu, gsig, geq, adv, hdr, s),
+          "advantage");
+  if (n_groups)
+    RLK_TRY(hipMemcpyAsync(n_groups, &hdr->n_groups, sizeof(int32_t), hipMemcpyDeviceToDevice, s), "copy n_groups");
+  return finish(hipSuccess, "", ws, s);
+}
+
+}  // namespace
 
 }  // namespace rlk
 
@@ -307,7 +384,8 @@ rlk_status_t rlk_logprob_fwd(const rlk_batch_t* b, const void* hidden, const voi
 
   RLK_TRY(launch_begin(reinterpret_cast<int32_t*>(hdr), b->cu_seqlens, b->R, N, s), "begin");
   if (N == 0) return finish(hipSuccess, "", ws, s);
-  RLK_TRY(launch_compact(mask, b->cu_seqlens, nullptr, b->R, N, targets, b->V, w, L, s), "compact");
+  RLK_TRY(launch_compact(mask, b->cu_seqlens, nullptr, b->R, N, targets, b->V, b->max_policy_tokens, w, L, s),
+          "compact");
   for (int c = 0; c < L.nchunks; ++c) {
     const int64_t c0 = (int64_t)c * L.Mc;
     RLK_TRY(launch_gather(b->dtype, hidden, b->d, reinterpret_cast<const int32_t*>(w + L.idx), hdr, c0, L.Mc,
@@ -378,7 +456,8 @@ rlk_status_t rlk_compact(const rlk_batch_t* b, const uint8_t* mask, const int32_
   char* w = static_cast<char*>(ws);
   WsHeader* hdr = reinterpret_cast<WsHeader*>(w + L.hdr);
   RLK_TRY(launch_begin(reinterpret_cast<int32_t*>(hdr), b->cu_seqlens, b->R, b->N, s), "begin");
-  RLK_TRY(launch_compact(mask, b->cu_seqlens, group_ids, b->R, b->N, targets, b->V, w, L, s), "compact");
+  RLK_TRY(launch_compact(mask, b->cu_seqlens, group_ids, b->R, b->N, targets, b->V, b->max_policy_tokens, w, L, s),
+          "compact");
   if (b->N > 0) {
     RLK_TRY(hipMemcpyAsync(idx, w + L.idx, (size_t)b->N * 4, hipMemcpyDeviceToDevice, s), "copy idx");
     RLK_TRY(hipMemcpyAsync(tok_rollout, w + L.tokr, (size_t)b->N * 4, hipMemcpyDeviceToDevice, s), "copy tok_rollout");
@@ -392,28 +471,11 @@ rlk_status_t rlk_compact(const rlk_batch_t* b, const uint8_t* mask, const int32_
 rlk_status_t rlk_group_advantage(int32_t R, const float* rewards, const int32_t* group_ids, float adv_eps,
                                  float* adv, int32_t* group_index, int32_t* n_groups, void* ws, size_t ws_bytes,
                                  void* stream) {
-  if (R < 0 || R > kMaxRollouts) return fail(RLK_ESHAPE, "R = %d outside [0, %d]", R, kMaxRollouts);
-  if (R > 0 && (!rewards || !group_ids || !adv)) return fail(RLK_EINVAL, "rewards, group_ids or adv is NULL");
-  if (!(adv_eps >= 0.0f) || !isfinite(adv_eps)) return fail(RLK_EINVAL, "adv_eps must be finite and >= 0");
-  rlk_status_t st = check_ws(ws, ws_bytes, advantage_ws_bytes(R));
+  rlk_status_t st = check_advantage_args(R, rewards, group_ids, adv_eps, adv);
   if (st) return st;
-  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
-  Alloc a;
-  char* w = static_cast<char*>(ws);
-  WsHeader* hdr = reinterpret_cast<WsHeader*>(w + a.take(sizeof(WsHeader)));
-  int32_t* first = reinterpret_cast<int32_t*>(w + a.take((size_t)R * 4));
-  int32_t* gidx_ws = reinterpret_cast<int32_t*>(w + a.take((size_t)R * 4));
-  int32_t* gsize = reinterpret_cast<int32_t*>(w + a.take((size_t)R * 4));
-  double* gmu = reinterpret_cast<double*>(w + a.take((size_t)R * 8));
-  double* gsig = reinterpret_cast<double*>(w + a.take((size_t)R * 8));
-  int32_t* geq = reinterpret_cast<int32_t*>(w + a.take((size_t)R * 4));
-  int32_t* gidx = group_index ? group_index : gidx_ws;
-  RLK_TRY(launch_begin(reinterpret_cast<int32_t*>(hdr), nullptr, 0, 0, s), "begin");
-  RLK_TRY(launch_advantage(R, rewards, group_ids, adv_eps, first, gidx, gsize, gmu, gsig, geq, adv, hdr, s),
-          "advantage");
-  if (n_groups)
-    RLK_TRY(hipMemcpyAsync(n_groups, &hdr->n_groups, sizeof(int32_t), hipMemcpyDeviceToDevice, s), "copy n_groups");
-  return finish(hipSuccess, "", ws, s);
+  st = check_ws(ws, ws_bytes, advantage_ws_bytes(R));
+  if (st) return st;
+  return advantage_call(R, rewards, group_ids, adv_eps, adv, group_index, n_groups, ws, stream);
 }
 
 rlk_status_t rlk_pg_loss_fwd_bwd(const rlk_batch_t* b, const void* hidden, const void* W, const int32_t* targets,
@@ -458,7 +520,8 @@ rlk_status_t rlk_pg_loss_fwd_bwd(const rlk_batch_t* b, const void* hidden, const
   auto I = [&](size_t off) { return reinterpret_cast<int32_t*>(w + off); };
 
   RLK_TRY(launch_begin(reinterpret_cast<int32_t*>(hdr), b->cu_seqlens, R, N, s), "begin");
-  RLK_TRY(launch_compact(mask, b->cu_seqlens, group_ids, R, N, targets, b->V, w, L, s), "compact");
+  RLK_TRY(launch_compact(mask, b->cu_seqlens, group_ids, R, N, targets, b->V, b->max_policy_tokens, w, L, s),
+          "compact");
   RLK_TRY(launch_advantage(R, rewards, group_ids, p->adv_eps, I(L.first), I(L.gidx), I(L.gsize),
                            reinterpret_cast<double*>(w + L.gmu), reinterpret_cast<double*>(w + L.gsig), I(L.geq),
                            F(L.adv), hdr, s),
@@ -735,11 +798,15 @@ int32_t rlk_version(void) { return RLK_VERSION; }
 rlk_status_t rlk_profile_begin(void) {
   Prof& P = prof();
   std::lock_guard<std::mutex> lk(P.mu);
-  for (auto& r : P.recs) {
-    (void)hipEventDestroy(r.a);
-    (void)hipEventDestroy(r.b);
-  }
   P.recs.clear();
+  P.next = 0;
+  P.open = nullptr;
+  P.open_kind = -1;
+  while (P.pool.size() < kProfPoolEvents) {
+    hipEvent_t ev;
+    if (hipEventCreate(&ev) != hipSuccess) return fail(RLK_EHIP, "hipEventCreate failed");
+    P.pool.push_back(ev);
+  }
   P.on = true;
   return RLK_OK;
 }
@@ -762,10 +829,9 @@ rlk_status_t rlk_profile_end(int32_t max_kinds, double* total_ms, int32_t* launc
       if (total_ms) total_ms[r.kind] += ms;
       if (launches) launches[r.kind] += 1;
     }
-    (void)hipEventDestroy(r.a);
-    (void)hipEventDestroy(r.b);
   }
   P.recs.clear();
+  P.next = 0;  // the events go back to the pool
   return rc;
 }
 

@@ -125,7 +125,8 @@ struct WsLayout {
 // ---- launchers (k_segment.hip) ----
 hipError_t launch_begin(int32_t* status_hdr, const int32_t* cu, int R, int64_t N, hipStream_t s);
 hipError_t launch_compact(const uint8_t* mask, const int32_t* cu, const int32_t* gid, int R, int64_t N,
-                          const int32_t* targets, int V, char* ws, const WsLayout& L, hipStream_t s);
+                          const int32_t* targets, int V, int32_t max_policy, char* ws, const WsLayout& L,
+                          hipStream_t s);
 hipError_t launch_advantage(int R, const float* rewards, const int32_t* gid, float adv_eps,
                             int32_t* first, int32_t* gidx, int32_t* gsize, double* gmu, double* gsig,
                             int32_t* geq, float* adv, WsHeader* hdr, hipStream_t s);

@@ -87,7 +87,8 @@ def aux_logps(inst, *, rollout_sigma=0.15, ref_sigma=0.3):
                 ref=torch.as_tensor(rf, device=dev))
 
 
-def run_gpu(inst, params, *, gid=None, mask="default", dW=None, ws=None, aux=None, token_adv=None, temperature=1.0):
+def run_gpu(inst, params, *, gid=None, mask="default", dW=None, ws=None, aux=None, token_adv=None, temperature=1.0,
+            max_policy_tokens=0):
     import torch
 
     h, W = inst["h"], inst["W"]
@@ -99,7 +100,7 @@ def run_gpu(inst, params, *, gid=None, mask="default", dW=None, ws=None, aux=Non
         h, W, inst["targets"], inst["mask"] if mask == "default" else mask, inst["cu"], inst["old"],
         inst["rewards"], inst["gid"] if gid is None else gid, params, dW=dW, logp_out=logp, entropy_out=ent,
         stats=stats, ws=ws, rollout_logp=aux["rollout"] if aux else None, ref_logp=aux["ref"] if aux else None,
-        token_adv=token_adv, temperature=temperature)
+        token_adv=token_adv, temperature=temperature, max_policy_tokens=max_policy_tokens)
     torch.cuda.synchronize()
     flags = rlk.check_status(ws)
     return dict(loss=float(loss.item()), dh=dh, dW=dWo, logp=logp, ent=ent, stats=rlk.stats_from_tensor(stats),

@@ -37,7 +37,7 @@ def test_exports_every_declared_symbol(lib):
 
 
 def test_version_and_strings(lib):
-    assert lib.rlk_version() == 4
+    assert lib.rlk_version() == 5
     assert lib.rlk_status_string(rlk.RLK_EWORKSPACE).decode().startswith("workspace")
     assert lib.rlk_kernel_kind_name(10).decode() == "fwd_lse_gemm"
 
@@ -127,7 +127,7 @@ def test_host_validation(lib):
         bad.temperature = tau
         assert lib.rlk_workspace_size(ctypes.byref(bad), None, ctypes.byref(n)) == rlk.RLK_EINVAL, tau
     bad = _batch(cfg)
-    bad.reserved = 1
+    bad.max_policy_tokens = -1
     assert lib.rlk_workspace_size(ctypes.byref(bad), None, ctypes.byref(n)) == rlk.RLK_EINVAL
     for tau in (0.0, 0.5, 2.0):
         ok = _batch(cfg)
@@ -172,3 +172,26 @@ def test_host_validation(lib):
         == rlk.RLK_EINVAL
     assert lib.rlk_group_advantage(8, None, fake, ctypes.c_float(1e-6), fake, None, None, fake, 1 << 20, None) \
         == rlk.RLK_EINVAL
+
+
+def test_policy_token_bound_sizes_the_chunks(lib):
+    # qwen8b shape: a bound on the trained tokens plans the chunk rows from it, within the same
+    # 256-row granularity and never above the unbounded chunk
+    cfg = get_config("qwen8b_bf16")
+    N = 524288
+    p = rlk.make_params()
+    free = rlk.workspace_size(_batch(cfg, N=N, R=128), p)
+    for bound in (211143, 100000, 40000, 1000):
+        b = _batch(cfg, N=N, R=128)
+        b.max_policy_tokens = bound
+        got = rlk.workspace_size(b, p)
+        assert 0 < got <= free, bound
+    small = _batch(cfg, N=N, R=128)
+    small.max_policy_tokens = 1000
+    assert rlk.workspace_size(small, p) < rlk.workspace_size(_batch(cfg, N=1280, R=128), p) * 2
+    # a bound above N is the same as N
+    b = _batch(cfg, N=N, R=128)
+    b.max_policy_tokens = N + 5
+    bN = _batch(cfg, N=N, R=128)
+    bN.max_policy_tokens = N
+    assert rlk.workspace_size(b, p) == rlk.workspace_size(bN, p)

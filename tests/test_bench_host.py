@@ -82,6 +82,40 @@ def test_occupancy_summary_recovers_clock_and_occupancy(tmp_path):
     assert abs(float(line[5]) - 0.25) < 1e-3    # waiting fraction
 
 
+def test_occupancy_summary_counts_executed_mfma_flops(tmp_path, monkeypatch):
+    # SQ_INSTS_VALU_MFMA_MOPS_BF16 counts 512-FLOP units over every launch, short ones included
+    monkeypatch.setattr(bench, "PROFILES", str(tmp_path))
+    rows = []
+    for did, (kind, mops, dur) in enumerate(((0, 1e9, 2_000_000), (1, 2e9, 3_000_000), (2, 3e9, 40_000))):
+        base = dict(Dispatch_Id=did, Kernel_Name=GEMM[kind], Start_Timestamp=0, End_Timestamp=dur)
+        rows += [dict(base, Counter_Name="GRBM_GUI_ACTIVE", Counter_Value=1e6 * bench.N_XCD),
+                 dict(base, Counter_Name="SQ_VALU_MFMA_BUSY_CYCLES", Counter_Value=5e5 * bench.N_SIMD),
+                 dict(base, Counter_Name="SQ_WAVE_CYCLES", Counter_Value=10.0),
+                 dict(base, Counter_Name="SQ_WAIT_ANY", Counter_Value=1.0),
+                 dict(base, Counter_Name="SQ_INSTS_VALU_MFMA_MOPS_BF16", Counter_Value=mops)]
+    p = tmp_path / "occ.csv"
+    _write_counters(p, rows)
+    text = bench.occupancy_summary(str(p), "t", "c")
+    (tmp_path / "gemm_occupancy_tiny_fp32.txt").write_text(text)
+    flop, occ = bench.read_occupancy("tiny_fp32", bench.kernel_source_digest())
+    assert flop == pytest.approx(6e9 * 512)
+    assert occ["fwd_lse_gemm"] == pytest.approx(0.5) and "dw_gemm" not in occ   # the 40 us launch is left out
+    assert bench.read_occupancy("tiny_fp32", "0" * 16) is None                     # other kernel sources
+
+
+def test_host_policy_token_count_and_cpu_ranges():
+    import numpy as np
+
+    class St:
+        cu_seqlens = np.array([0, 3, 5, 9])
+        mask = np.array([1, 0, 1, 1, 1, 0, 1, 1, 0], np.uint8)
+        group_ids = np.array([4, -1, 4])
+
+    assert bench.host_policy_tokens(St) == 4
+    assert bench.host_policy_tokens(St, exclusion=False) == 6
+    assert bench._ranges([0, 1, 2, 3, 8, 10, 11]) == "0-3,8,10-11"
+
+
 def _traffic_rows(counter, copy_kib, gemm_kib, dz_kib):
     rows = [dict(Dispatch_Id=1, Kernel_Name=COPY, Counter_Name=counter, Counter_Value=copy_kib,
                  Start_Timestamp=0, End_Timestamp=1)]

@@ -277,6 +277,30 @@ def test_device_data_errors_are_flagged():
     assert run_gpu(inst, p)["flags"] == 0
 
 
+@pytest.mark.parametrize("name,chunk", [("qwen8b_bf16", 512), ("large_bf16", 256), ("tiny_fp32", 0)])
+def test_policy_token_bound(name, chunk):
+    """A host-known bound on the trained tokens sizes the chunk loop: exact and loose bounds give the
+    oracle's results, per-token outputs and dhidden bitwise equal to the unbounded call (rows do not
+    depend on the chunking); a bound below the batch's count is flagged."""
+    import torch
+
+    cfg = WL.scaled_config(name) if name != "tiny_fp32" else WL.get_config(name)
+    inst = build_instance(cfg)
+    p = params_for(cfg, chunk_rows=chunk)
+    free = run_gpu(inst, p)
+    n_eff = int(free["stats"]["n_policy_tokens"])
+    ref = run_oracle(inst, p)
+    for bound in (n_eff, n_eff + 777):
+        log(f"bound {cfg.name}: n_eff={n_eff} max_policy_tokens={bound} chunk_rows={chunk}")
+        got = run_gpu(inst, p, max_policy_tokens=bound)
+        compare_full(inst, got, ref, p, tag=f"bound {bound}")
+        assert got["loss"] == free["loss"]
+        assert torch.equal(got["logp"], free["logp"]) and torch.equal(got["dh"], free["dh"])
+        assert rel_fro(to_host(got["dW"]), to_host(free["dW"])) <= 1e-5
+    log(f"bound {cfg.name}: max_policy_tokens={n_eff - 1} (below the count)")
+    assert run_gpu(inst, p, max_policy_tokens=n_eff - 1)["flags"] & rlk.DERR_POLICY_BOUND
+
+
 # ------------------------------------------------------------------ full-size, sampled rows
 class _CompactRows:
     """Compacted policy rows of a device tensor, fetched to the host block by block."""
