@@ -182,6 +182,20 @@ rlk_status_t rlk_group_advantage(int32_t R, const float* rewards, const int32_t*
                                  float adv_eps, float* adv, int32_t* group_index,
                                  int32_t* n_groups, void* ws, size_t ws_bytes, void* stream);
 
+/* rlk_group_advantage without a workspace argument, for callers that cannot allocate device memory
+ * (code under HIP graph capture, tight serving loops, harnesses that forbid hipMalloc).  Same
+ * arguments, computation and results; the workspace is a fixed device array inside the library of
+ * the size rlk_group_advantage needs for 16384 rollouts (524,544 bytes), one copy per device, held
+ * by each GPU the library runs on until the process ends.  R above 16384 returns RLK_ESHAPE before
+ * anything is launched; `stream` must belong to the current device (RLK_EINVAL otherwise).  Nothing
+ * is allocated: no hipMalloc, hipFree or allocating library call.  Every call on one GPU uses that
+ * GPU's array, so calls that overlap on one GPU (other streams or host threads) race: the caller
+ * serialises them.  No part of the array has to start at zero (the first launch resets the status
+ * word, later ones write every entry they read). */
+rlk_status_t rlk_group_advantage_noalloc(int32_t R, const float* rewards, const int32_t* group_ids,
+                                         float adv_eps, float* adv, int32_t* group_index,
+                                         int32_t* n_groups, void* stream);
+
 /* Masked clipped policy-gradient loss, forward and backward (Sec. 2.3.1-2.3.2,
  * Sec. 3.2.3, Sec. 3.3, Sec. 3.4), with the log-prob forward inside.
  *   loss      device float[1]: L = -objective under p->agg.

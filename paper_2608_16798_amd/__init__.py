@@ -24,6 +24,7 @@ EXPORTS = [
     "rlk_pg_loss_fwd_bwd", "rlk_check_status", "rlk_status_string", "rlk_last_error", "rlk_version",
     "rlk_profile_begin", "rlk_profile_end", "rlk_kernel_kind_name", "rlk_gae", "rlk_value_workspace_size",
     "rlk_value_loss", "rlk_tree_pack", "rlk_value_head_fwd", "rlk_value_head_workspace_size", "rlk_value_head_bwd",
+    "rlk_group_advantage_noalloc",
 ]
 
 
@@ -85,6 +86,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.rlk_compact.argtypes = [pb, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
     lib.rlk_logprob_fwd.argtypes = [pb, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
     lib.rlk_group_advantage.argtypes = [i32, vp, vp, f32, vp, vp, vp, vp, sz, vp]
+    lib.rlk_group_advantage_noalloc.argtypes = [i32, vp, vp, f32, vp, vp, vp, vp]
     lib.rlk_pg_loss_fwd_bwd.argtypes = [pb, vp, vp, vp, vp, vp, vp, vp, pp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
     lib.rlk_check_status.argtypes = [vp, vp, ctypes.POINTER(i32)]
     lib.rlk_status_string.argtypes = [i32]
@@ -330,6 +332,28 @@ def group_advantage(rewards, group_ids, adv_eps=1e-6, adv=None, group_index=None
     _on_one_gpu(rewards=rewards, group_ids=group_ids, adv=adv, group_index=group_index, n_groups=n_groups, ws=ws)
     _check(lib.rlk_group_advantage(R, _ptr(rewards), _ptr(group_ids), adv_eps, _ptr(adv), _ptr(group_index),
                                    _ptr(n_groups), _ptr(ws), ws.numel(), _stream_handle(stream)))
+    return adv
+
+
+def group_advantage_noalloc(rewards, group_ids, adv_eps=1e-6, adv=None, group_index=None, n_groups=None,
+                            stream=None):
+    """group_advantage through rlk_group_advantage_noalloc: the library's fixed device scratch instead
+    of a workspace (for callers that cannot allocate; calls overlapping on one GPU race)."""
+    import torch
+
+    _tensor(rewards, "rewards", shape=(None,), dtypes=(torch.float32,))
+    R = rewards.shape[0]
+    _tensor(group_ids, "group_ids", shape=(R,), dtypes=(torch.int32,))
+    _tensor(adv, "adv", shape=(R,), dtypes=(torch.float32,), optional=True)
+    _tensor(group_index, "group_index", shape=(R,), dtypes=(torch.int32,), optional=True)
+    _tensor(n_groups, "n_groups", shape=(None,), dtypes=(torch.int32,), optional=True, min_bytes=4)
+    _on_one_gpu(rewards=rewards, group_ids=group_ids, adv=adv, group_index=group_index, n_groups=n_groups)
+    lib = load_library()
+    if adv is None:
+        adv = torch.empty(R, dtype=torch.float32, device=rewards.device)
+    _on_one_gpu(rewards=rewards, adv=adv)
+    _check(lib.rlk_group_advantage_noalloc(R, _ptr(rewards), _ptr(group_ids), adv_eps, _ptr(adv), _ptr(group_index),
+                                           _ptr(n_groups), _stream_handle(stream)))
     return adv
 
 

@@ -338,6 +338,42 @@ rlk_status_t advantage_call(int32_t R, const float* rewards, const int32_t* grou
   return finish(hipSuccess, "", ws, s);
 }
 
+// ---------------------------------------------------------------- fixed device scratch
+// Workspace of rlk_group_advantage_noalloc: the advantage workspace of the largest supported rollout
+// count, one copy per device, held by every GPU the library runs on until the process ends.  On the
+// host, `scratch` names a host-side stand-in, never the device memory: host code only uses the
+// device address that hipGetSymbolAddress returns for the current device, looked up once per device.
+constexpr size_t kAdvScratchBytes = advantage_ws_bytes(kMaxRollouts);
+static __device__ __align__(256) char scratch[kAdvScratchBytes];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+// Device address of `scratch` on the device of `stream`, which must be the current device.
+rlk_status_t device_scratch(void* stream, void** out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  if (stream) {
+    hipDevice_t sdev = 0;
+    e = hipStreamGetDevice(reinterpret_cast<hipStream_t>(stream), &sdev);
+    if (e != hipSuccess) return hip_fail(e, "hipStreamGetDevice");
+    if ((int)sdev != dev) return fail(RLK_EINVAL, "the stream belongs to device %d, the current device is %d", (int)sdev, dev);
+  }
+  if (dev < 0 || dev >= kMaxDevices) return fail(RLK_EINVAL, "device %d outside [0, %d)", dev, kMaxDevices);
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return hip_fail(e, "hipGetSymbolAddress(scratch)");
+    if (!p || (reinterpret_cast<uintptr_t>(p) & 255) != 0) return fail(RLK_EHIP, "scratch address is not 256-aligned");
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return RLK_OK;
+}
+
 }  // namespace
 
 }  // namespace rlk
@@ -474,6 +510,19 @@ rlk_status_t rlk_group_advantage(int32_t R, const float* rewards, const int32_t*
   rlk_status_t st = check_advantage_args(R, rewards, group_ids, adv_eps, adv);
   if (st) return st;
   st = check_ws(ws, ws_bytes, advantage_ws_bytes(R));
+  if (st) return st;
+  return advantage_call(R, rewards, group_ids, adv_eps, adv, group_index, n_groups, ws, stream);
+}
+
+rlk_status_t rlk_group_advantage_noalloc(int32_t R, const float* rewards, const int32_t* group_ids, float adv_eps,
+                                         float* adv, int32_t* group_index, int32_t* n_groups, void* stream) {
+  rlk_status_t st = check_advantage_args(R, rewards, group_ids, adv_eps, adv);
+  if (st) return st;
+  if (advantage_ws_bytes(R) > kAdvScratchBytes)
+    return fail(RLK_ESHAPE, "R = %d needs %zu bytes of scratch, the fixed array holds %zu", R, advantage_ws_bytes(R),
+                kAdvScratchBytes);
+  void* ws = nullptr;
+  st = device_scratch(stream, &ws);
   if (st) return st;
   return advantage_call(R, rewards, group_ids, adv_eps, adv, group_index, n_groups, ws, stream);
 }
