@@ -428,6 +428,20 @@ def next_rows(cfg, inp, params, steps):
     out["value_head_fwd_TBps"] = rate(n_eff * d * esz, t_hf)          # read the policy rows
     out["value_head_bwd_ms"] = round(t_hb, 4)
     out["value_head_bwd_TBps"] = rate(N * d * esz + n_eff * d * esz, t_hb)  # read policy rows, write all rows
+    # group-relative advantages (sort + segmented reduction) at the batch's R and at the largest
+    # supported rollout count, 16384 rollouts in groups of 8 under shuffled keys
+    adv_r = torch.empty(R, dtype=torch.float32, device=dev)
+    aws = rlk.alloc_workspace(rlk.advantage_workspace_size(R), dev)
+    out["advantage_ms"] = round(timed(lambda: rlk.group_advantage(inp["rewards"], inp["gid"], 1e-6, adv=adv_r, ws=aws),
+                                      20), 4)
+    Rm = 16384
+    rng_a = np.random.default_rng(cfg.seed + 78)
+    gid_m = torch.as_tensor(rng_a.permutation(np.repeat(np.arange(Rm // 8), 8)).astype(np.int32) * 7 + 3, device=dev)
+    rew_m = torch.as_tensor(rng_a.random(Rm).astype(np.float32), device=dev)
+    adv_m = torch.empty(Rm, dtype=torch.float32, device=dev)
+    aws_m = rlk.alloc_workspace(rlk.advantage_workspace_size(Rm), dev)
+    out["advantage_16384_rollouts_ms"] = round(timed(lambda: rlk.group_advantage(rew_m, gid_m, 1e-6, adv=adv_m, ws=aws_m),
+                                                     20), 4)
     # host prefix-tree packer: 128 rollouts of 8 calls; each call's context is the previous history
     # (prompt, responses, tool observations), and every fourth rollout repeats one call
     rng = np.random.default_rng(cfg.seed + 77)

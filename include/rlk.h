@@ -185,7 +185,7 @@ rlk_status_t rlk_group_advantage(int32_t R, const float* rewards, const int32_t*
 /* rlk_group_advantage without a workspace argument, for callers that cannot allocate device memory
  * (code under HIP graph capture, tight serving loops, harnesses that forbid hipMalloc).  Same
  * arguments, computation and results; the workspace is a fixed device array inside the library of
- * the size rlk_group_advantage needs for 16384 rollouts (524,544 bytes), one copy per device, held
+ * the size rlk_group_advantage needs for 16384 rollouts (590,336 bytes), one copy per device, held
  * by each GPU the library runs on until the process ends.  R above 16384 returns RLK_ESHAPE before
  * anything is launched; `stream` must belong to the current device (RLK_EINVAL otherwise).  Nothing
  * is allocated: no hipMalloc, hipFree or allocating library call.  Every call on one GPU uses that

@@ -71,11 +71,13 @@ class RlkError(RuntimeError):
 _lib = None
 
 
-def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
-    """Load librlk.so (raises if it has not been built)."""
+def load_library(path: Optional[str] = None) -> ctypes.CDLL:
+    """Load librlk.so (raises if it has not been built).  RLK_LIBRARY (environment) names another
+    build of the same library, e.g. the host-sanitizer build librlk_hostsan.so."""
     global _lib
     if _lib is not None:
         return _lib
+    path = path or os.environ.get("RLK_LIBRARY") or LIB_PATH
     if not os.path.exists(path):
         raise RuntimeError(f"librlk.so not found at {path}; build it with `python -m paper_2608_16798_amd.build`")
     lib = ctypes.CDLL(path)

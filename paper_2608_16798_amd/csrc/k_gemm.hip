@@ -247,6 +247,11 @@ __global__ void __launch_bounds__(NT) k_gemm(GemmArgs a) {
     voa[j] = (uint32_t)(lane / CPR) * lda_b + chunk * 16;
     vob[j] = (uint32_t)(lane / CPR) * ldb_b + chunk * 16;
   }
+  // Rows past the panel (ragged last tiles) read as zero because their vector offset alone is out of
+  // range: 0x80000000 >= num_records (every 256-row panel is at most 2 GiB, checked by the host), so
+  // the read stays inside the panel whether or not the hardware adds the scalar offset to the check.
+  // A lane's row is r0 + lane / CPR; it is past the panel when r0 >= rows - lane / CPR.
+  const int lim_a = rows_a - lane / CPR, lim_b = rows_b - lane / CPR;
   // copies of slice kt for the rows owned by wavefront w
   auto dma_w = [&](int kt, int w) {
     char* st = smem + (kt % NSTAGE) * STAGE_B;
@@ -254,7 +259,8 @@ __global__ void __launch_bounds__(NT) k_gemm(GemmArgs a) {
 #pragma unroll
     for (int j = 0; j < IPW; ++j) {
       const uint32_t r0 = (uint32_t)((w * IPW + j) * RPI);
-      uint32_t oa = voa[j & 1], ob = vob[j & 1];
+      uint32_t oa = (int)r0 < lim_a ? voa[j & 1] : 0x80000000u;
+      uint32_t ob = (int)r0 < lim_b ? vob[j & 1] : 0x80000000u;
       if constexpr (KTAIL) {
         // chunks past the end of K would read the next row: push them out of range (zero fill)
         const int row = (w * IPW + j) * RPI + lane / CPR;

@@ -197,91 +197,127 @@ k_rollout_offsets(const int32_t* cu, int R, int64_t N, const int32_t* idx, const
 }
 
 // ---- group-relative advantages ----
+//
+// Segmentation by sorting: the (key, rollout) pairs of the non-excluded rollouts are sorted in one
+// workgroup (bitonic network in LDS, R <= kMaxRollouts), so each group becomes a run of consecutive
+// entries with its members in ascending rollout order; a scan over the run starts gives the dense
+// group index (the rank of the key among the sorted distinct keys).  The statistics are then a
+// segmented reduction: one wavefront per run.  O(R log^2 R) work for the sort, O(R) for the rest.
 
-__global__ void __launch_bounds__(kThreads) k_group_first(const int32_t* gid, int R, int32_t* first) {
-  const int r = blockIdx.x * blockDim.x + threadIdx.x;
-  if (r >= R) return;
-  const int32_t key = gid[r];
-  int f = key >= 0 ? 1 : 0;
-  for (int j = 0; j < r && f; ++j)
-    if (gid[j] == key) f = 0;
-  first[r] = f;
+constexpr int kSortThreads = 1024;
+constexpr int kSortMax = 16384;  // = kMaxRollouts: 128 KiB of 64-bit sort entries in LDS
+static_assert(kSortMax >= kMaxRollouts, "sort capacity");
+
+// entry = (key' << 32) | rollout with key' = key for a kept rollout and 0xFFFFFFFF for an excluded one
+// (and for the padding), so kept rollouts sort first, by key, then by rollout.
+__device__ inline uint64_t sort_entry(const int32_t* gid, int R, int i) {
+  if (i >= R) return ~0ull;
+  const int32_t key = gid[i];
+  const uint32_t hi = key >= 0 ? (uint32_t)key : 0xFFFFFFFFu;
+  return ((uint64_t)hi << 32) | (uint32_t)i;
 }
 
-__global__ void __launch_bounds__(kThreads)
-k_group_rank(const int32_t* gid, int R, const int32_t* first, int32_t* gidx, WsHeader* hdr) {
-  const int r = blockIdx.x * blockDim.x + threadIdx.x;
-  if (r < R) {
-    const int32_t key = gid[r];
-    int rank = -1;
-    if (key >= 0) {
-      rank = 0;
-      for (int j = 0; j < R; ++j) rank += (first[j] && gid[j] < key) ? 1 : 0;
+__global__ void __launch_bounds__(kSortThreads)
+k_group_sort(const int32_t* gid, int R, int32_t* members, int32_t* gstart, int32_t* gidx, WsHeader* hdr) {
+  __shared__ uint64_t e[kSortMax];
+  __shared__ int wsum[kSortThreads / 64];
+  __shared__ int carry_s;
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  int P = 1;
+  while (P < R) P <<= 1;
+  for (int i = tid; i < P; i += kSortThreads) e[i] = sort_entry(gid, R, i);
+  __syncthreads();
+  // bitonic sort of P entries, ascending
+  for (int k = 2; k <= P; k <<= 1) {
+    for (int j = k >> 1; j > 0; j >>= 1) {
+      for (int i = tid; i < P; i += kSortThreads) {
+        const int l = i ^ j;
+        if (l > i) {
+          const uint64_t a = e[i], b = e[l];
+          const bool up = (i & k) == 0;
+          if ((a > b) == up) {
+            e[i] = b;
+            e[l] = a;
+          }
+        }
+      }
+      __syncthreads();
     }
-    gidx[r] = rank;
   }
-  if (blockIdx.x == 0) {
-    __shared__ int sq[kThreads / 64], sv[kThreads / 64];
-    int q = 0, v = 0;
-    for (int j = threadIdx.x; j < R; j += blockDim.x) {
-      q += first[j];
-      v += gid[j] >= 0 ? 1 : 0;
-    }
-    q = wave_sum(q);
-    v = wave_sum(v);
-    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-    if (lane == 0) { sq[w] = q; sv[w] = v; }
+  // kept entries come first; a run starts where the key differs from the previous entry's
+  if (tid == 0) carry_s = 0;
+  __syncthreads();
+  for (int base = 0; base < R; base += kSortThreads) {
+    const int i = base + tid;
+    const uint64_t v = i < R ? e[i] : ~0ull;
+    const bool kept = (v >> 32) != 0xFFFFFFFFull;
+    const int start = kept && (i == 0 || (e[i - 1] >> 32) != (v >> 32)) ? 1 : 0;
+    const int inc = wave_inclusive_scan(start, lane);
+    if (lane == 63) wsum[w] = inc;
     __syncthreads();
-    if (threadIdx.x == 0) {
-      int a = 0, b = 0;
-      for (int i = 0; i < kThreads / 64; ++i) { a += sq[i]; b += sv[i]; }
-      hdr->n_groups = a;
-      hdr->n_valid = b;
+    int off = carry_s;
+    for (int j = 0; j < w; ++j) off += wsum[j];
+    const int q = off + inc - 1;  // dense index of this entry's group
+    if (kept) {
+      const int r = (int)(uint32_t)v;
+      members[i] = r;
+      gidx[r] = q;
+      if (start) gstart[q] = i;
+    } else if (i < R) {
+      gidx[(int)(uint32_t)v] = -1;
     }
+    __syncthreads();
+    if (tid == kSortThreads - 1) carry_s = off + inc;
+    __syncthreads();
+  }
+  // n_valid = number of kept entries: the first excluded (or padding) position
+  if (tid == 0) {
+    int lo = 0, hi = R;
+    while (lo < hi) {
+      const int mid = (lo + hi) >> 1;
+      if ((e[mid] >> 32) != 0xFFFFFFFFull) lo = mid + 1; else hi = mid;
+    }
+    gstart[carry_s] = lo;  // end of the last run
+    hdr->n_groups = carry_s;
+    hdr->n_valid = lo;
   }
 }
 
-// One wavefront per group: members visited in ascending rollout order, fixed shuffle tree.
+// Segmented statistics: one wavefront per group over its members (ascending rollout order), lanes
+// striding the run, partial sums combined by a fixed shuffle tree: mean and population std in
+// fp64, and whether every reward of the group is bitwise equal.
 __global__ void __launch_bounds__(kThreads)
-k_group_stats(const float* rewards, const int32_t* gidx, int R, const WsHeader* hdr, int32_t* gsize,
-              double* gmu, double* gsig, int32_t* geq) {
+k_group_stats(const float* rewards, const int32_t* members, const int32_t* gstart, const WsHeader* hdr,
+              int32_t* gsize, double* gmu, double* gsig, int32_t* geq) {
   const int lane = threadIdx.x & 63;
   const int q = blockIdx.x * (kThreads / 64) + (threadIdx.x >> 6);
   if (q >= hdr->n_groups) return;
+  const int b = gstart[q], n = gstart[q + 1] - b;
   double sum = 0.0;
-  int cnt = 0;
   float mn = INFINITY, mx = -INFINITY;
-  for (int base = 0; base < R; base += 64) {
-    int r = base + lane;
-    if (r < R && gidx[r] == q) {
-      float v = rewards[r];
-      sum += (double)v;
-      cnt += 1;
-      mn = fminf(mn, v);
-      mx = fmaxf(mx, v);
-    }
+  for (int i = lane; i < n; i += 64) {
+    const float v = rewards[members[b + i]];
+    sum += (double)v;
+    mn = fminf(mn, v);
+    mx = fmaxf(mx, v);
   }
   sum = wave_sum(sum);
-  cnt = wave_sum(cnt);
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) {
     mn = fminf(mn, __shfl_xor(mn, o, 64));
     mx = fmaxf(mx, __shfl_xor(mx, o, 64));
   }
-  const double mu = cnt > 0 ? sum / (double)cnt : 0.0;
+  const double mu = n > 0 ? sum / (double)n : 0.0;
   double ss = 0.0;
-  for (int base = 0; base < R; base += 64) {
-    int r = base + lane;
-    if (r < R && gidx[r] == q) {
-      double dv = (double)rewards[r] - mu;
-      ss += dv * dv;
-    }
+  for (int i = lane; i < n; i += 64) {
+    const double dv = (double)rewards[members[b + i]] - mu;
+    ss += dv * dv;
   }
   ss = wave_sum(ss);
   if (lane == 0) {
-    gsize[q] = cnt;
+    gsize[q] = n;
     gmu[q] = mu;
-    gsig[q] = cnt > 0 ? sqrt(ss / (double)cnt) : 0.0;
+    gsig[q] = n > 0 ? sqrt(ss / (double)n) : 0.0;
     geq[q] = (mn == mx) ? 1 : 0;
   }
 }
@@ -340,16 +376,16 @@ hipError_t launch_compact(const uint8_t* mask, const int32_t* cu, const int32_t*
   return hipGetLastError();
 }
 
-hipError_t launch_advantage(int R, const float* rewards, const int32_t* gid, float adv_eps, int32_t* first,
-                            int32_t* gidx, int32_t* gsize, double* gmu, double* gsig, int32_t* geq,
+hipError_t launch_advantage(int R, const float* rewards, const int32_t* gid, float adv_eps, int32_t* members,
+                            int32_t* gstart, int32_t* gidx, int32_t* gsize, double* gmu, double* gsig, int32_t* geq,
                             float* adv, WsHeader* hdr, hipStream_t s) {
   if (R <= 0) return hipSuccess;
+  if (R > kSortMax) return hipErrorInvalidValue;
   prof_mark(KK_GROUP_RANK, true, s);
-  k_group_first<<<blocks_for(R, kThreads), kThreads, 0, s>>>(gid, R, first);
-  k_group_rank<<<blocks_for(R, kThreads), kThreads, 0, s>>>(gid, R, first, gidx, hdr);
+  k_group_sort<<<1, kSortThreads, 0, s>>>(gid, R, members, gstart, gidx, hdr);
   prof_mark(KK_GROUP_RANK, false, s);
   prof_mark(KK_GROUP_STATS, true, s);
-  k_group_stats<<<blocks_for(R, kThreads / 64), kThreads, 0, s>>>(rewards, gidx, R, hdr, gsize, gmu, gsig,
+  k_group_stats<<<blocks_for(R, kThreads / 64), kThreads, 0, s>>>(rewards, members, gstart, hdr, gsize, gmu, gsig,
                                                                    geq);
   prof_mark(KK_GROUP_STATS, false, s);
   prof_mark(KK_ADVANTAGE, true, s);

@@ -179,7 +179,8 @@ rlk_status_t layout(const rlk_batch_t* b, bool bwd, int64_t chunk_rows, WsLayout
   L.et = a.take((size_t)N * 4);
   L.rstart = a.take((size_t)R * 4);
   L.rnpol = a.take((size_t)R * 4);
-  L.first = a.take((size_t)R * 4);
+  L.members = a.take((size_t)R * 4);
+  L.gstart = a.take((size_t)(R + 1) * 4);
   L.gidx = a.take((size_t)R * 4);
   L.gsize = a.take((size_t)R * 4);
   L.gmu = a.take((size_t)R * 8);
@@ -205,6 +206,12 @@ rlk_status_t layout(const rlk_batch_t* b, bool bwd, int64_t chunk_rows, WsLayout
     const size_t pb = std::max(splitk_bytes(Mc, d, L.sk_dh), splitk_bytes(V, d, L.sk_dw));
     if (pb > 0) L.part = a.take(pb);
   }
+  // The GEMMs address each 256-row operand panel with 32-bit buffer offsets and mark rows past a
+  // ragged panel with the offset 0x80000000: every panel must span at most 2 GiB.
+  const int64_t lds[] = {d, L.ldq, L.ldt, L.ldw};
+  for (int64_t ld : lds)
+    if ((int64_t)kTile * ld * esz > ((int64_t)1 << 31))
+      return fail(RLK_ESHAPE, "a %d-row operand panel of row stride %lld exceeds 2 GiB", kTile, (long long)ld);
   L.total = a.off;
   return RLK_OK;
 }
@@ -212,7 +219,8 @@ rlk_status_t layout(const rlk_batch_t* b, bool bwd, int64_t chunk_rows, WsLayout
 constexpr size_t advantage_ws_bytes(int32_t R) {
   Alloc a;
   a.take(sizeof(WsHeader));
-  a.take((size_t)R * 4);  // first
+  a.take((size_t)R * 4);        // members
+  a.take((size_t)(R + 1) * 4);  // run starts
   a.take((size_t)R * 4);  // gidx
   a.take((size_t)R * 4);  // gsize
   a.take((size_t)R * 8);  // mu
@@ -323,7 +331,8 @@ rlk_status_t advantage_call(int32_t R, const float* rewards, const int32_t* grou
   Alloc a;
   char* w = static_cast<char*>(ws);
   WsHeader* hdr = reinterpret_cast<WsHeader*>(w + a.take(sizeof(WsHeader)));
-  int32_t* first = reinterpret_cast<int32_t*>(w + a.take((size_t)R * 4));
+  int32_t* members = reinterpret_cast<int32_t*>(w + a.take((size_t)R * 4));
+  int32_t* gstart = reinterpret_cast<int32_t*>(w + a.take((size_t)(R + 1) * 4));
   int32_t* gidx_ws = reinterpret_cast<int32_t*>(w + a.take((size_t)R * 4));
   int32_t* gsize = reinterpret_cast<int32_t*>(w + a.take((size_t)R * 4));
   double* gmu = reinterpret_cast<double*>(w + a.take((size_t)R * 8));
@@ -331,7 +340,7 @@ rlk_status_t advantage_call(int32_t R, const float* rewards, const int32_t* grou
   int32_t* geq = reinterpret_cast<int32_t*>(w + a.take((size_t)R * 4));
   int32_t* gidx = group_index ? group_index : gidx_ws;
   RLK_TRY(launch_begin(reinterpret_cast<int32_t*>(hdr), nullptr, 0, 0, s), "begin");
-  RLK_TRY(launch_advantage(R, rewards, group_ids, adv_eps, first, gidx, gsize, gmu, gsig, geq, adv, hdr, s),
+  RLK_TRY(launch_advantage(R, rewards, group_ids, adv_eps, members, gstart, gidx, gsize, gmu, gsig, geq, adv, hdr, s),
           "advantage");
   if (n_groups)
     RLK_TRY(hipMemcpyAsync(n_groups, &hdr->n_groups, sizeof(int32_t), hipMemcpyDeviceToDevice, s), "copy n_groups");
@@ -344,6 +353,7 @@ rlk_status_t advantage_call(int32_t R, const float* rewards, const int32_t* grou
 // host, `scratch` names a host-side stand-in, never the device memory: host code only uses the
 // device address that hipGetSymbolAddress returns for the current device, looked up once per device.
 constexpr size_t kAdvScratchBytes = advantage_ws_bytes(kMaxRollouts);
+static_assert(kAdvScratchBytes == 590336, "the size stated in rlk.h");
 static __device__ __align__(256) char scratch[kAdvScratchBytes];
 
 constexpr int kMaxDevices = 64;
@@ -571,7 +581,7 @@ rlk_status_t rlk_pg_loss_fwd_bwd(const rlk_batch_t* b, const void* hidden, const
   RLK_TRY(launch_begin(reinterpret_cast<int32_t*>(hdr), b->cu_seqlens, R, N, s), "begin");
   RLK_TRY(launch_compact(mask, b->cu_seqlens, group_ids, R, N, targets, b->V, b->max_policy_tokens, w, L, s),
           "compact");
-  RLK_TRY(launch_advantage(R, rewards, group_ids, p->adv_eps, I(L.first), I(L.gidx), I(L.gsize),
+  RLK_TRY(launch_advantage(R, rewards, group_ids, p->adv_eps, I(L.members), I(L.gstart), I(L.gidx), I(L.gsize),
                            reinterpret_cast<double*>(w + L.gmu), reinterpret_cast<double*>(w + L.gsig), I(L.geq),
                            F(L.adv), hdr, s),
           "advantage");

@@ -101,7 +101,7 @@ struct WsLayout {
   // compaction block scan [nblk]
   size_t blkcnt = 0, blkoff = 0;
   // rollouts [R]
-  size_t rstart = 0, rnpol = 0, first = 0, gidx = 0, gsize = 0, gmu = 0, gsig = 0, geq = 0, adv = 0;
+  size_t rstart = 0, rnpol = 0, members = 0, gstart = 0, gidx = 0, gsize = 0, gmu = 0, gsig = 0, geq = 0, adv = 0;
   size_t rsum = 0;  // double [R][kRollSums]
   // chunk buffers
   size_t pm = 0, ps = 0, pu = 0;   // float [nvt][Mc]
@@ -127,9 +127,11 @@ hipError_t launch_begin(int32_t* status_hdr, const int32_t* cu, int R, int64_t N
 hipError_t launch_compact(const uint8_t* mask, const int32_t* cu, const int32_t* gid, int R, int64_t N,
                           const int32_t* targets, int V, int32_t max_policy, char* ws, const WsLayout& L,
                           hipStream_t s);
-hipError_t launch_advantage(int R, const float* rewards, const int32_t* gid, float adv_eps,
-                            int32_t* first, int32_t* gidx, int32_t* gsize, double* gmu, double* gsig,
-                            int32_t* geq, float* adv, WsHeader* hdr, hipStream_t s);
+// members [R] (rollouts of the kept groups, group by group), gstart [R + 1] (run starts), gidx [R],
+// and per group gsize, gmu, gsig, geq [R]; R <= kMaxRollouts.
+hipError_t launch_advantage(int R, const float* rewards, const int32_t* gid, float adv_eps, int32_t* members,
+                            int32_t* gstart, int32_t* gidx, int32_t* gsize, double* gmu, double* gsig, int32_t* geq,
+                            float* adv, WsHeader* hdr, hipStream_t s);
 
 // ---- launchers (k_token.hip) ----
 hipError_t launch_transpose_w(int dtype, const void* W, void* WT, int V, int64_t Vp, int d, int64_t ldw,
