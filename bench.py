@@ -590,7 +590,7 @@ def main():
     if rlk.check_status(ws) != 0:
         raise SystemExit("device data error in the benchmark batch")
     n_eff = host_policy_tokens(st, exclusion=not args.logprob_only)
-    if not args.logprob_only:
+    if not args.logprob_only and args.warmup > 0:
         s = rlk.stats_from_tensor(stats)
         if int(s["n_policy_tokens"]) != n_eff:
             raise SystemExit(f"policy tokens: device {int(s['n_policy_tokens'])}, host {n_eff}")
