@@ -276,7 +276,7 @@ def read_occupancy(workload: str, digest: str):
     return flop, occ
 
 
-HBM_KERNELS = ("k_dz", "k_gather", "k_transpose_w", "k_zero_fill", "k_combine")
+HBM_KERNELS = ("k_dz", "k_gather", "k_target_logit", "k_hidden_t", "k_transpose_w", "k_zero_fill", "k_combine")
 
 
 def hbm_kernel_summary(fetch_csv, write_csv, workload, copy_mib, cmd_fetch, cmd_write):
@@ -294,10 +294,18 @@ def hbm_kernel_summary(fetch_csv, write_csv, workload, copy_mib, cmd_fetch, cmd_
     n_eff = int(np.asarray(st.mask, dtype=np.int64).sum())
     esz = 2 if cfg.dtype == "bf16" else 4
     vp = (cfg.V + 255) // 256 * 256
-    alg = {"k_dz": 3 * n_eff * vp * esz, "k_gather": 3 * n_eff * cfg.d * esz,
+    # token-reference layout (bf16 without an entropy term): no explicit dz pass unless a chunk is
+    # flagged, the gather writes h_c only, and the s-scaled h_c^T comes after the combine
+    ref = cfg.dtype == "bf16" and cfg.entropy_coef == 0.0
+    hrow = n_eff * cfg.d * esz
+    alg = {"k_dz": 0 if ref else 3 * n_eff * vp * esz, "k_gather": (2 if ref else 3) * hrow,
+           "k_target_logit": 2 * hrow, "k_hidden_t": 2 * hrow,
            "k_transpose_w": (cfg.V + vp) * cfg.d * esz, "k_zero_fill": (st.N - n_eff) * (cfg.d * esz + 8),
            "k_combine": n_eff * (12 * (vp // 256) + 40)}
-    what = {"k_dz": "read q, write dz and dz^T", "k_gather": "read h rows, write h_c and h_c^T",
+    what = {"k_dz": "none: no chunk flagged (token-reference layout)" if ref else "read q, write dz and dz^T",
+            "k_gather": "read h rows, write h_c" + ("" if ref else " and h_c^T"),
+            "k_target_logit": "read h_c rows and the target rows of W",
+            "k_hidden_t": "read h_c, write the row-scaled h_c^T",
             "k_transpose_w": "read W, write W^T", "k_zero_fill": "zero untrained rows of dh, logp, entropy",
             "k_combine": "read the online-LSE partials, write per-token values"}
 
@@ -327,8 +335,8 @@ def hbm_kernel_summary(fetch_csv, write_csv, workload, copy_mib, cmd_fetch, cmd_
             if k not in fetch or k not in write:
                 continue
             hbm = (sum(fetch[k].values()) * kf + sum(write[k].values()) * kw) * 1024.0
-            f.write(f"{k:15s} {len(fetch[k]):8d} {hbm / 1e9:9.3f} {alg[k] / 1e9:9.3f} {hbm / alg[k]:6.3f}  "
-                    f"{what[k]}\n")
+            ratio = f"{hbm / alg[k]:6.3f}" if alg[k] else f"{'-':>6s}"
+            f.write(f"{k:15s} {len(fetch[k]):8d} {hbm / 1e9:9.3f} {alg[k] / 1e9:9.3f} {ratio}  {what[k]}\n")
     return path
 
 
@@ -671,6 +679,11 @@ def main():
         cpu = cpu_baseline(cfg, inp, args.cpu_tokens, n_eff)
         log(f"[bench] oracle {cpu['value']:.1f} policy tokens/s in {cpu['seconds']:.1f} s")
 
+    dz_chunks = None
+    if not args.logprob_only:
+        s = rlk.stats_from_tensor(stats)
+        dz_chunks = {"explicit_dz": int(s["n_dz_chunks"]), "chunks": int(s["n_chunks"])}
+
     metric = METRIC if not args.logprob_only else "policy tokens/sec for the logprob forward (pi_old pass); % of bf16 MFMA peak"
     out = {
         "metric": metric, "value": round(value, 1), "unit": "policy tokens/s", "n_gpus": 1, "steps": args.steps,
@@ -682,7 +695,7 @@ def main():
         "timing": {"ms_per_step_median": round(ms_per_step, 3), "ms_per_step_mean": round(float(np.mean(step_ms)), 3),
                    "ms_per_step_min": round(float(np.min(step_ms)), 3), "ms_per_step_max": round(float(np.max(step_ms)), 3),
                    "ms_wall_per_step": round((t1 - t0) * 1e3 / args.steps, 3),
-                   "per_kernel_events": use_events},
+                   "per_kernel_events": use_events, "dz_chunks": dz_chunks},
         "mfma_pct_of_peak": round(100 * mfma_frac, 2),
         "executed_mfma_pct": executed["pct_of_peak"] if executed else None, "executed_mfma": executed,
         "roofline": roofline, "cpu_baseline": cpu, "kernels": per_kernel,

@@ -48,7 +48,7 @@
 extern "C" {
 #endif
 
-#define RLK_VERSION 5
+#define RLK_VERSION 6
 
 typedef int32_t rlk_status_t;
 enum {
@@ -140,6 +140,9 @@ typedef struct {
   int64_t n_policy_tokens;/* N_eff */
   float kl_mean;          /* token mean of the sampled-token KL estimate (0 when off) */
   float tis_mean;         /* token mean of the importance weight w_t (1 when off) */
+  int32_t n_chunks;       /* chunk iterations of the call */
+  int32_t n_dz_chunks;    /* chunks whose logit gradient dz was formed explicitly (see
+                           * rlk_pg_loss_fwd_bwd); the others applied dz = diag(s) q in the GEMMs */
 } rlk_pg_stats_t;
 
 /* Workspace bytes needed by rlk_logprob_fwd (p == NULL) or by rlk_pg_loss_fwd_bwd (p
@@ -205,7 +208,13 @@ rlk_status_t rlk_group_advantage_noalloc(int32_t R, const float* rewards, const 
  *             current policy on trained rows, 0 elsewhere.
  *   stats     device rlk_pg_stats_t or NULL.
  * old_logp [N] fp32 is read on trained rows only.  With no trainable token the loss is 0,
- * dhidden is 0 and an overwritten dW is 0. */
+ * dhidden is 0 and an overwritten dW is 0.
+ * The logit gradient is dz_tj = g_t ([j = y_t] - p_tj) (plus the entropy term when
+ * entropy_coef != 0).  For bf16 without an entropy term the stored probabilities are taken
+ * against each token's target logit, which makes dz = diag(s) q with q the stored values (target
+ * entry adjusted), so the dhidden and dW GEMMs apply the row scale s and dz is never written; a
+ * chunk holding a token with a target far below its largest logits (log-prob below about -40)
+ * forms dz explicitly instead, with the same result.  stats->n_dz_chunks counts those chunks. */
 rlk_status_t rlk_pg_loss_fwd_bwd(const rlk_batch_t* b, const void* hidden, const void* W,
                                  const int32_t* targets, const uint8_t* mask,
                                  const float* old_logp, const float* rewards,

@@ -46,7 +46,8 @@ class PgStats(ctypes.Structure):
     _fields_ = [("loss", ctypes.c_float), ("pg_loss", ctypes.c_float), ("entropy_mean", ctypes.c_float),
                 ("clip_frac", ctypes.c_float), ("ratio_mean", ctypes.c_float), ("n_groups", ctypes.c_int32),
                 ("n_valid_rollouts", ctypes.c_int32), ("n_policy_tokens", ctypes.c_int64),
-                ("kl_mean", ctypes.c_float), ("tis_mean", ctypes.c_float)]
+                ("kl_mean", ctypes.c_float), ("tis_mean", ctypes.c_float), ("n_chunks", ctypes.c_int32),
+                ("n_dz_chunks", ctypes.c_int32)]
 
 
 class Calls(ctypes.Structure):

@@ -198,6 +198,18 @@ __device__ __forceinline__ bool map_tile(int tm, int tn, int& tile_m, int& tile_
 constexpr int LDS_DEEP_B = 5 * OPND_B;
 static_assert(LDS_DEEP_B <= 163840 && LDS_DEEP_B >= LDS_B, "three-stage pipeline fits the LDS");
 
+// Reference of the stored probabilities of chunk column n in a forward tile with maximum m: m itself,
+// or with a.zr (token-reference layout) the column's reference logit r, clamped to m - kRefSpan where
+// it lies further below (then, with mark, the chunk is flagged: its dz needs the explicit pass).
+// Columns n >= N (padding) keep m.
+__device__ __forceinline__ float tile_ref(const GemmArgs& a, float m, int n, int N, bool mark) {
+  if (!a.zr || n >= N) return m;
+  const float r = a.zr[n];
+  if (r >= m - kRefSpan) return r;
+  if (mark) *a.fb = 1;
+  return m - kRefSpan;
+}
+
 template <typename T, int EPI, bool STORE_Q, bool KTAIL>
 __global__ void __launch_bounds__(NT) k_gemm(GemmArgs a) {
   constexpr bool DEEP_B = EPI == EPI_FWD && sizeof(T) == 2;
@@ -501,7 +513,9 @@ __global__ void __launch_bounds__(NT) k_gemm(GemmArgs a) {
     }
     __syncthreads();
 
-    // phase 2: e = exp(z - m), s = sum e, u = sum e (z - m); e optionally staged for storage.
+    // phase 2: e = exp(z - c), s = sum e, u = sum e (z - c) against the token's reference c (the
+    // tile maximum m, or with a.zr the reference logit r clamped to m - kRefSpan); e optionally
+    // staged for storage.
     char* sQ = smem;
 #pragma unroll
     for (int nb = 0; nb < NBW; ++nb) {
@@ -509,7 +523,8 @@ __global__ void __launch_bounds__(NT) k_gemm(GemmArgs a) {
       float mt = red_m[cl];
 #pragma unroll
       for (int w = 1; w < WAVES_M; ++w) mt = fmaxf(mt, red_m[w * kTile + cl]);
-      const float mt2 = mt * kLog2e;
+      const float ref = tile_ref(a, mt, tile_n * kTile + cl, N, true);
+      const float mt2 = ref * kLog2e;
       float s = 0.0f, u = 0.0f;
 #pragma unroll
       for (int mb = 0; mb < MBW; ++mb)
@@ -524,7 +539,7 @@ __global__ void __launch_bounds__(NT) k_gemm(GemmArgs a) {
             const bool valid = full_v || v0 + rl < V;
             const float e = valid ? __builtin_amdgcn_exp2f(fmaf(z, kLog2e, -mt2)) : 0.0f;
             s += e;
-            u = fmaf(e, z - mt, u);
+            u = fmaf(e, z - ref, u);
             ev[i] = e;
           }
           if constexpr (STORE_Q) {
@@ -566,7 +581,7 @@ __global__ void __launch_bounds__(NT) k_gemm(GemmArgs a) {
             u += red_u[w * kTile + cl];
           }
           const int64_t o = (int64_t)tile_m * a.Mc + n;
-          a.pm[o] = m;
+          a.pm[o] = tile_ref(a, m, n, N, false);
           a.ps[o] = s;
           a.pu[o] = u;
         }
@@ -587,10 +602,41 @@ __global__ void __launch_bounds__(NT) k_gemm(GemmArgs a) {
           __builtin_nontemporal_store(v, reinterpret_cast<u32x4*>(dst));
         }
       }
+      if (a.qt) {
+        // phase 4: the same tile transposed into q^T[v0 .. v0 + 255][tokens of the tile], the dW
+        // GEMM's operand (columns of tokens >= N as zero).  Each lane transposes an 8 x 8 square in
+        // registers: wavefront w covers 64 x 64 blocks w and w + 8, lane (a8, b8) the vocabulary
+        // rows 8 a8 .. + 7 and tokens 8 b8 .. + 7 of a block.  The LDS reads of 8 consecutive lanes
+        // span one 128-byte row segment (conflict free); each store writes 8 full 128-byte lines.
+        const int a8 = lane & 7, b8 = lane >> 3;
+#pragma unroll
+        for (int it = 0; it < kTile * kTile / 4096 / NWAVE; ++it) {
+          const int blk = wid + NWAVE * it;
+          const int rl0 = (blk & 3) * 64 + a8 * 8, cl0 = (blk >> 2) * 64 + b8 * 8;
+          const int n0 = tile_n * kTile + cl0;
+          u32x4 in[8];
+#pragma unroll
+          for (int j = 0; j < 8; ++j)
+            in[j] = n0 + j < N ? *reinterpret_cast<const u32x4*>(sQ + (cl0 + j) * QROW + rl0 * 2) : u32x4{0, 0, 0, 0};
+#pragma unroll
+          for (int k = 0; k < 8; ++k) {
+            u32x4 o;
+#pragma unroll
+            for (int m = 0; m < 4; ++m) {
+              const uint32_t lo = in[2 * m][k >> 1], hi = in[2 * m + 1][k >> 1];
+              o[m] = (k & 1) ? ((lo >> 16) | (hi & 0xffff0000u)) : ((lo & 0xffffu) | (hi << 16));
+            }
+            char* dst = reinterpret_cast<char*>(a.qt) + ((int64_t)(v0 + rl0 + k) * a.ldqt + n0) * 2;
+            __builtin_nontemporal_store(o, reinterpret_cast<u32x4*>(dst));
+          }
+        }
+      }
     }
   } else if constexpr (EPI == EPI_DH) {
     // rows = chunk-local tokens, columns = hidden features; scatter to dh[idx[c0 + row]].
+    // With row scales (token-reference layout), dh = diag(s) (q W^T).
     T* out = reinterpret_cast<T*>(a.out);
+    const bool scaled = a.rs != nullptr && *a.rs_off == 0;
 #pragma unroll
     for (int mb = 0; mb < MBW; ++mb)
 #pragma unroll
@@ -598,10 +644,11 @@ __global__ void __launch_bounds__(NT) k_gemm(GemmArgs a) {
         const int rl = tile_m * kTile + wm * WTM + mb * 32 + (r >> 2) * 8 + lh * 4 + (r & 3);
         if (rl < M) {
           const int64_t row = a.idx[a.c0 + rl];
+          const float sc = scaled ? a.rs[rl] : 1.0f;
 #pragma unroll
           for (int nb = 0; nb < NBW; ++nb) {
             const int cl = tile_n * kTile + wn * WTN + nb * 32 + lrow;
-            if (cl < N) store_elem<T>(out + row * a.ldo + cl, acc[mb][nb][r]);
+            if (cl < N) store_elem<T>(out + row * a.ldo + cl, acc[mb][nb][r] * sc);
           }
         }
       }
@@ -646,6 +693,7 @@ __global__ void __launch_bounds__(256) k_splitk_reduce(GemmArgs a) {
     for (int y = 0; y < a.ksplit; ++y) acc += a.part[((int64_t)y * a.mp + m) * a.ldp + n];
     if constexpr (EPI == EPI_DH) {
       const int64_t row = a.idx[a.c0 + m];
+      if (a.rs && *a.rs_off == 0) acc *= a.rs[m];
       store_elem<T>(reinterpret_cast<T*>(a.out) + row * a.ldo + n, acc);
     } else {
       float* p = a.dw + m * a.ldo + n;

@@ -63,6 +63,8 @@ __global__ void __launch_bounds__(kThreads) k_begin(WsHeader* hdr, const int32_t
     hdr->n_eff = 0;
     hdr->n_groups = 0;
     hdr->n_valid = 0;
+    hdr->ref_fallback = 0;
+    hdr->n_dz_chunks = 0;
   }
 }
 

@@ -19,6 +19,7 @@ namespace rlk {
 namespace {
 
 constexpr float kLog2e = 1.4426950408889634f;
+constexpr int64_t kDzBlocks = 8192;  // dz launch: 32 per CU, looping over the chunk's block tiles
 
 __device__ __forceinline__ float bf16_to_f(uint16_t b) { return __uint_as_float(((uint32_t)b) << 16); }
 __device__ __forceinline__ uint16_t f_to_bf16(float x) { return __builtin_bit_cast(uint16_t, (__bf16)x); }
@@ -139,6 +140,75 @@ k_gather(const T* hidden, int d, const int32_t* idx, const WsHeader* hdr, int64_
   }
 }
 
+// ---- reference logits of the token-reference layout (bf16): zr[t] = (hc[t] . W[y_t]) / tau, one
+// wavefront per chunk row, fp32 sums of 16-byte loads.  Block 0 also clears the chunk's flag.
+__global__ void __launch_bounds__(256) k_target_logit(const uint16_t* hc, int d, const uint16_t* W,
+                                                      const int32_t* ytgt, const WsHeader* hdr, int64_t c0,
+                                                      int64_t Mc, int V, float inv_tau, float* zr, int32_t* fb) {
+  if (blockIdx.x == 0 && threadIdx.x == 0) *fb = 0;
+  int64_t rc = (int64_t)hdr->n_eff - c0;
+  rc = rc < 0 ? 0 : (rc > Mc ? Mc : rc);
+  const int lane = threadIdx.x & 63;
+  const int64_t t = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (t >= rc) return;
+  const int y = ytgt[c0 + t];
+  float acc = 0.0f;
+  if (y >= 0 && y < V) {
+    const uint16_t* h = hc + t * d;
+    const uint16_t* w = W + (int64_t)y * d;
+    for (int j = lane * 8; j < d; j += 512) {
+      const u32x4 x = *reinterpret_cast<const u32x4*>(h + j);
+      const u32x4 v = *reinterpret_cast<const u32x4*>(w + j);
+#pragma unroll
+      for (int k = 0; k < 8; ++k) acc = fmaf(vget<uint16_t>(x, k), vget<uint16_t>(v, k), acc);
+    }
+  }
+  acc = wave_sum(acc);
+  if (lane == 0) zr[t] = acc * inv_tau;
+}
+
+// ---- HT[j][t] = hc[t][j] * s_t for the dW GEMM of the token-reference layout (s_t = 1 when the
+// chunk is flagged); zero columns t in [rows, K pad).  64 x 64 tiles through LDS as in k_gather.
+__global__ void __launch_bounds__(256) k_hidden_t(const uint16_t* hc, int d, const float* st, const int32_t* fb,
+                                                  const WsHeader* hdr, int64_t c0, int64_t Mc, uint16_t* ht,
+                                                  int64_t ldt) {
+  __shared__ __attribute__((aligned(16))) uint16_t tile[64][64 + 8];
+  int64_t rc = (int64_t)hdr->n_eff - c0;
+  rc = rc < 0 ? 0 : (rc > Mc ? Mc : rc);
+  const int64_t rpad = (rc + kKAlign - 1) / kKAlign * kKAlign;
+  const int64_t t0 = (int64_t)blockIdx.x * 64;
+  const int j0 = blockIdx.y * 64;
+  if (t0 >= rpad) return;
+  const bool scaled = *fb == 0;
+  for (int c = threadIdx.x; c < 64 * 8; c += 256) {
+    const int tl = c / 8, ch = c % 8;
+    const int64_t t = t0 + tl;
+    const int j = j0 + ch * 8;
+    u32x4 v = u32x4{0, 0, 0, 0};
+    if (t < rc && j < d) {
+      v = *reinterpret_cast<const u32x4*>(hc + t * d + j);
+      if (scaled) {
+        const float sc = st[t];
+        uint16_t e[8];
+#pragma unroll
+        for (int k = 0; k < 8; ++k) e[k] = f_to_bf16(vget<uint16_t>(v, k) * sc);
+        v = vpack<uint16_t>(e);
+      }
+    }
+    *reinterpret_cast<u32x4*>(&tile[tl][ch * 8]) = v;
+  }
+  __syncthreads();
+  for (int c = threadIdx.x; c < 64 * 8; c += 256) {
+    const int jl = c / 8, ch = c % 8;
+    const int j = j0 + jl;
+    if (j >= d) continue;
+    uint16_t vals[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) vals[i] = tile[ch * 8 + i][jl];
+    *reinterpret_cast<u32x4*>(ht + (int64_t)j * ldt + t0 + ch * 8) = vpack<uint16_t>(vals);
+  }
+}
+
 // ---- merge of the per-vocabulary-tile partials (m, s, u) into lse, logp, H; loss scalars.
 __global__ void __launch_bounds__(256) k_combine(TokenParams p) {
   // 64 tokens per block; wavefront w merges the vocabulary tiles k = w, w + 4, ... of its lane's
@@ -225,18 +295,37 @@ __global__ void __launch_bounds__(256) k_combine(TokenParams p) {
     // KL term: d/dlogp of -beta (e^r - r - 1), r = ref - logp, is beta (e^r - 1)
     if (p.ref_logp) dlogp += (double)p.kl_coef * (double)expm1f(p.ref_logp[row] - logp);
     // g, e are taken per raw logit W h: the temperature's 1 / tau enters here, once
-    p.gt[i] = (float)(w * dlogp * (double)p.inv_tau);
+    const float g = (float)(w * dlogp * (double)p.inv_tau);
+    p.gt[i] = g;
     p.et[i] = (float)(w * (double)p.ent_coef * (double)p.inv_tau);
+    if (p.zr) {
+      // Token-reference layout: q_tj = exp(z_tj - r), so dz_tj = -g p_tj = s q_tj with
+      // s = -g exp(r - lse), except at the target, where dz = g (1 - p_y) = -g expm1(logp): its
+      // entry of q and q^T becomes expm1(logp) exp(lse - r), and dz = diag(s) q holds exactly.
+      const float r = p.zr[tl];
+      const float sc = -g * expf(r - lsef);
+      const float qy = expm1f(logp) * expf(lsef - r);
+      p.st[tl] = sc;
+      if (!(fabsf(qy) <= kRefQMax) || (sc != 0.0f && !(fabsf(sc) >= kRefSMin))) *p.fb = 1;
+      const int y = p.ytgt[i];
+      if (y >= 0 && y < p.V) {
+        const uint16_t qb = f_to_bf16(qy);
+        reinterpret_cast<uint16_t*>(p.q)[tl * p.ldq + y] = qb;
+        reinterpret_cast<uint16_t*>(p.qt)[(int64_t)y * p.ldqt + tl] = qb;
+      }
+    }
   }
 }
 
-// ---- dz for a chunk: q holds exp(z - m_tile) per (token, vocabulary); rewritten in place with
-// dz and also written transposed for the dW GEMM.  Block tile: 64 tokens x 256 vocabulary
-// entries (one forward vocabulary tile, so one m_tile per token).  Each thread owns an EPC x EPC
+// ---- dz for a chunk: q holds exp(z - c) per (token, vocabulary) against the reference c = pm of
+// its (token, vocabulary tile); rewritten in place with dz and also written transposed for the dW
+// GEMM.  Block tile: 64 tokens x 256 vocabulary entries (one forward vocabulary tile, so one c
+// per token); the blocks of the launch loop over the chunk's tiles.  Each thread owns an EPC x EPC
 // square (EPC tokens x EPC consecutive vocabulary entries, EPC = elements per 16 bytes): it reads
 // EPC 16-byte rows, writes them back as dz and transposes the square in registers into EPC
 // 16-byte rows of dz^T, so neither layout needs an LDS pass.  The per-token scalars are
-// computed once per block into LDS.
+// computed once per block tile into LDS.  With p.fb the launch does nothing unless the chunk is
+// flagged (token-reference layout: dz = diag(s) q is applied by the GEMMs instead).
 template <typename T, bool ENT>
 __global__ void __launch_bounds__(256) k_dz(DzParams p) {
   constexpr int EPC = 16 / sizeof(T);
@@ -246,81 +335,87 @@ __global__ void __launch_bounds__(256) k_dz(DzParams p) {
   constexpr int PASSES = kVocabTile / (4 * VSPAN);
   __shared__ float s_sc[64], s_g[64], s_e[64], s_base[64], s_dzy[64];
   __shared__ int s_y[64], s_ok[64];   // s_ok: token inside the chunk (else dz = 0)
+  if (p.fb && *p.fb == 0) return;
+  if (p.ndz && blockIdx.x == 0 && threadIdx.x == 0) atomicAdd(p.ndz, 1);
   int64_t rc = (int64_t)p.hdr->n_eff - p.c0;
   rc = rc < 0 ? 0 : (rc > p.Mc ? p.Mc : rc);
   const int64_t rpad = (rc + kKAlign - 1) / kKAlign * kKAlign;
-  const int vt = blockIdx.x;
-  const int64_t v0 = (int64_t)vt * kVocabTile;
-  const int64_t t0 = (int64_t)blockIdx.y * 64;
-  if (t0 >= rpad) return;
-  if (threadIdx.x < 64) {
-    const int tl = threadIdx.x;
-    const int64_t t = t0 + tl;
-    float sc = 0.0f, g = 0.0f, e = 0.0f, base = 0.0f, dzy = 0.0f;
-    int y = -1;
-    if (t < rc) {
-      const int64_t i = p.c0 + t;
-      const float lse = p.lse[i], logp = p.logp[i], H = p.ent[i];
-      g = p.gt[i];
-      e = p.et[i];
-      const float mk = p.pm[(int64_t)vt * p.Mc + t];
-      sc = __builtin_amdgcn_exp2f((mk - lse) * kLog2e);
-      base = mk - lse + H;    // z - lse + H = log q + base
-      const int yy = p.ytgt[i];
-      if (yy >= v0 && yy < v0 + kVocabTile) y = (int)(yy - v0);
-      // the target entry uses the exact fp32 log-prob: 1 - p_y = -expm1(logp)
-      dzy = g * (-expm1f(logp));
-      if (ENT) dzy -= e * expf(logp) * (logp + H);
+  const int nvt = (int)(p.Vp / kVocabTile);
+  const int64_t nbt = (int64_t)nvt * (rpad / 64);
+  for (int64_t bt = blockIdx.x; bt < nbt; bt += gridDim.x) {
+    const int vt = (int)(bt % nvt);
+    const int64_t v0 = (int64_t)vt * kVocabTile;
+    const int64_t t0 = bt / nvt * 64;
+    if (threadIdx.x < 64) {
+      const int tl = threadIdx.x;
+      const int64_t t = t0 + tl;
+      float sc = 0.0f, g = 0.0f, e = 0.0f, base = 0.0f, dzy = 0.0f;
+      int y = -1;
+      if (t < rc) {
+        const int64_t i = p.c0 + t;
+        const float lse = p.lse[i], logp = p.logp[i], H = p.ent[i];
+        g = p.gt[i];
+        e = p.et[i];
+        const float mk = p.pm[(int64_t)vt * p.Mc + t];
+        sc = __builtin_amdgcn_exp2f((mk - lse) * kLog2e);
+        base = mk - lse + H;    // z - lse + H = log q + base
+        const int yy = p.ytgt[i];
+        if (yy >= v0 && yy < v0 + kVocabTile) y = (int)(yy - v0);
+        // the target entry uses the exact fp32 log-prob: 1 - p_y = -expm1(logp)
+        dzy = g * (-expm1f(logp));
+        if (ENT) dzy -= e * expf(logp) * (logp + H);
+      }
+      s_sc[tl] = sc;
+      s_g[tl] = g;
+      s_e[tl] = e;
+      s_base[tl] = base;
+      s_dzy[tl] = dzy;
+      s_y[tl] = y;
+      s_ok[tl] = t < rc;
     }
-    s_sc[tl] = sc;
-    s_g[tl] = g;
-    s_e[tl] = e;
-    s_base[tl] = base;
-    s_dzy[tl] = dzy;
-    s_y[tl] = y;
-    s_ok[tl] = t < rc;
-  }
-  __syncthreads();
-  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
-  const int vc = lane % VC, tg = lane / VC;
-  T* q = reinterpret_cast<T*>(p.q);
-  T* dzt = reinterpret_cast<T*>(p.dzt);
+    __syncthreads();
+    const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+    const int vc = lane % VC, tg = lane / VC;
+    T* q = reinterpret_cast<T*>(p.q);
+    T* dzt = reinterpret_cast<T*>(p.dzt);
 #pragma unroll
-  for (int ps = 0; ps < PASSES; ++ps) {
-    const int vl0 = (ps * 4 + wid) * VSPAN + vc * EPC;   // tile-local first vocabulary entry
-    u32x4 raw[EPC];
+    for (int ps = 0; ps < PASSES; ++ps) {
+      const int vl0 = (ps * 4 + wid) * VSPAN + vc * EPC;   // tile-local first vocabulary entry
+      u32x4 raw[EPC];
 #pragma unroll
-    for (int j = 0; j < EPC; ++j)
-      raw[j] = *reinterpret_cast<const u32x4*>(q + (t0 + tg * EPC + j) * p.ldq + v0 + vl0);
-    float o[EPC][EPC];
+      for (int j = 0; j < EPC; ++j)
+        raw[j] = *reinterpret_cast<const u32x4*>(q + (t0 + tg * EPC + j) * p.ldq + v0 + vl0);
+      float o[EPC][EPC];
 #pragma unroll
-    for (int j = 0; j < EPC; ++j) {
-      const int tl = tg * EPC + j;
-      const float sc = s_sc[tl], g = s_g[tl];
-      const int y = s_y[tl];
-      const bool ok = s_ok[tl] != 0;
+      for (int j = 0; j < EPC; ++j) {
+        const int tl = tg * EPC + j;
+        const float sc = s_sc[tl], g = s_g[tl];
+        const int y = s_y[tl];
+        const bool ok = s_ok[tl] != 0;
+#pragma unroll
+        for (int k = 0; k < EPC; ++k) {
+          const float qv = vget<T>(raw[j], k);
+          float coef = g;
+          if (ENT) coef += (qv > 0.0f) ? s_e[tl] * (__logf(qv) + s_base[tl]) : 0.0f;
+          o[j][k] = !ok ? 0.0f : (vl0 + k == y) ? s_dzy[tl] : -(qv * sc) * coef;
+        }
+      }
+#pragma unroll
+      for (int j = 0; j < EPC; ++j) {
+        T row[EPC];
+#pragma unroll
+        for (int k = 0; k < EPC; ++k) row[k] = to_storage<T>(o[j][k]);
+        *reinterpret_cast<u32x4*>(q + (t0 + tg * EPC + j) * p.ldq + v0 + vl0) = vpack<T>(row);
+      }
 #pragma unroll
       for (int k = 0; k < EPC; ++k) {
-        const float qv = vget<T>(raw[j], k);
-        float coef = g;
-        if (ENT) coef += (qv > 0.0f) ? s_e[tl] * (__logf(qv) + s_base[tl]) : 0.0f;
-        o[j][k] = !ok ? 0.0f : (vl0 + k == y) ? s_dzy[tl] : -(qv * sc) * coef;
+        T col[EPC];
+#pragma unroll
+        for (int j = 0; j < EPC; ++j) col[j] = to_storage<T>(o[j][k]);
+        *reinterpret_cast<u32x4*>(dzt + (v0 + vl0 + k) * p.ldt + t0 + tg * EPC) = vpack<T>(col);
       }
     }
-#pragma unroll
-    for (int j = 0; j < EPC; ++j) {
-      T row[EPC];
-#pragma unroll
-      for (int k = 0; k < EPC; ++k) row[k] = to_storage<T>(o[j][k]);
-      *reinterpret_cast<u32x4*>(q + (t0 + tg * EPC + j) * p.ldq + v0 + vl0) = vpack<T>(row);
-    }
-#pragma unroll
-    for (int k = 0; k < EPC; ++k) {
-      T col[EPC];
-#pragma unroll
-      for (int j = 0; j < EPC; ++j) col[j] = to_storage<T>(o[j][k]);
-      *reinterpret_cast<u32x4*>(dzt + (v0 + vl0 + k) * p.ldt + t0 + tg * EPC) = vpack<T>(col);
-    }
+    __syncthreads();  // the next block tile rewrites the per-token scalars
   }
 }
 
@@ -430,6 +525,8 @@ __global__ void __launch_bounds__(1024) k_loss_final(LossParams p) {
       st.n_groups = Q;
       st.n_valid_rollouts = p.hdr->n_valid;
       st.n_policy_tokens = n_eff;
+      st.n_chunks = p.nchunks;
+      st.n_dz_chunks = p.hdr->n_dz_chunks;
       *p.stats = st;
     }
   }
@@ -482,6 +579,25 @@ hipError_t launch_gather(int dtype, const void* hidden, int d, const int32_t* id
   return hipGetLastError();
 }
 
+hipError_t launch_target_logit(const void* hc, int d, const void* W, const int32_t* ytgt, const WsHeader* hdr,
+                               int64_t c0, int64_t Mc, int V, float inv_tau, float* zr, int32_t* fb,
+                               hipStream_t s) {
+  prof_mark(KK_TARGET_LOGIT, true, s);
+  k_target_logit<<<(unsigned)((Mc + 3) / 4), 256, 0, s>>>((const uint16_t*)hc, d, (const uint16_t*)W, ytgt, hdr, c0,
+                                                          Mc, V, inv_tau, zr, fb);
+  prof_mark(KK_TARGET_LOGIT, false, s);
+  return hipGetLastError();
+}
+
+hipError_t launch_hidden_t(const void* hc, int d, const float* st, const int32_t* fb, const WsHeader* hdr,
+                           int64_t c0, int64_t Mc, void* ht, int64_t ldt, hipStream_t s) {
+  dim3 grid((unsigned)((Mc + 63) / 64), (unsigned)((d + 63) / 64));
+  prof_mark(KK_HIDDEN_T, true, s);
+  k_hidden_t<<<grid, 256, 0, s>>>((const uint16_t*)hc, d, st, fb, hdr, c0, Mc, (uint16_t*)ht, ldt);
+  prof_mark(KK_HIDDEN_T, false, s);
+  return hipGetLastError();
+}
+
 hipError_t launch_combine(const TokenParams& p, hipStream_t s) {
   prof_mark(KK_COMBINE, true, s);
   k_combine<<<(unsigned)((p.Mc + 63) / 64), 256, 0, s>>>(p);
@@ -490,7 +606,8 @@ hipError_t launch_combine(const TokenParams& p, hipStream_t s) {
 }
 
 hipError_t launch_dz(int dtype, const DzParams& p, hipStream_t s) {
-  dim3 grid((unsigned)(p.Vp / kVocabTile), (unsigned)(p.Mc / 64));
+  const int64_t nbt = p.Vp / kVocabTile * (p.Mc / 64);
+  const unsigned grid = (unsigned)(nbt < kDzBlocks ? nbt : kDzBlocks);
   prof_mark(KK_DZ, true, s);
   if (dtype == RLK_DTYPE_BF16) {
     if (p.has_ent) k_dz<uint16_t, true><<<grid, 256, 0, s>>>(p);

@@ -19,7 +19,7 @@ namespace rlk {
 // Layouts the Python binding mirrors.
 static_assert(sizeof(rlk_batch_t) == 40, "rlk_batch_t layout");
 static_assert(sizeof(rlk_pg_params_t) == 72, "rlk_pg_params_t layout");
-static_assert(sizeof(rlk_pg_stats_t) == 48, "rlk_pg_stats_t layout");
+static_assert(sizeof(rlk_pg_stats_t) == 56, "rlk_pg_stats_t layout");
 
 namespace {
 
@@ -200,6 +200,8 @@ rlk_status_t layout(const rlk_batch_t* b, bool bwd, int64_t chunk_rows, WsLayout
     L.q = a.take((size_t)(Mc * L.ldq * esz));
     L.dzt = a.take((size_t)(L.Vp * L.ldt * esz));
     L.wt = a.take((size_t)(d * L.ldw * esz));
+    L.zr = a.take((size_t)Mc * 4);
+    L.st = a.take((size_t)Mc * 4);
     // split-K partials of the dhidden and dW GEMMs (used one after the other)
     L.sk_dh = splitk_plan(Mc, d, L.Vp * esz);
     L.sk_dw = splitk_plan(V, d, Mc * esz);
@@ -290,7 +292,7 @@ const char* kKindNames[KK_COUNT_KINDS] = {
     "begin",        "compact_count", "compact_scan",  "compact_write", "rollout_offsets", "group_rank",
     "group_stats",  "advantage",     "transpose_w",   "gather",        "fwd_lse_gemm",    "lse_combine",
     "dz",           "dh_gemm",       "dw_gemm",       "loss_rollout",  "loss_final",      "zero_fill",
-    "gae",          "value_loss",    "value_head"};
+    "gae",          "value_loss",    "value_head",    "target_logit",  "hidden_t"};
 
 }  // namespace
 
@@ -586,10 +588,21 @@ rlk_status_t rlk_pg_loss_fwd_bwd(const rlk_batch_t* b, const void* hidden, const
                            F(L.adv), hdr, s),
           "advantage");
   RLK_TRY(launch_transpose_w(b->dtype, W, w + L.wt, b->V, L.Vp, b->d, L.ldw, s), "transpose_w");
+  // Token-reference layout (bf16 without an entropy term): the forward stores q against each token's
+  // target logit and writes q^T as well; the combine makes dz = diag(s) q exact, the dhidden GEMM and
+  // the scaled transpose of the gathered rows apply s, and the explicit dz pass runs only for chunks
+  // flagged on the device (a token whose target lies too far below its largest logits).
+  const bool ref_layout = b->dtype == RLK_DTYPE_BF16 && p->entropy_coef == 0.0f;
+  int32_t* fb = &hdr->ref_fallback;
   for (int c = 0; c < L.nchunks; ++c) {
     const int64_t c0 = (int64_t)c * L.Mc;
-    RLK_TRY(launch_gather(b->dtype, hidden, b->d, I(L.idx), hdr, c0, L.Mc, w + L.hc, w + L.ht, L.ldt, true, s),
+    RLK_TRY(launch_gather(b->dtype, hidden, b->d, I(L.idx), hdr, c0, L.Mc, w + L.hc, w + L.ht, L.ldt, !ref_layout,
+                          s),
             "gather");
+    if (ref_layout)
+      RLK_TRY(launch_target_logit(w + L.hc, b->d, W, I(L.ytgt), hdr, c0, L.Mc, b->V, inv_temperature(b), F(L.zr),
+                                  fb, s),
+              "target_logit");
     GemmArgs g = {};
     g.A = W;
     g.B = w + L.hc;
@@ -610,6 +623,12 @@ rlk_status_t rlk_pg_loss_fwd_bwd(const rlk_batch_t* b, const void* hidden, const
     g.ldq = L.ldq;
     g.V = b->V;
     g.inv_tau = inv_temperature(b);
+    if (ref_layout) {
+      g.zr = F(L.zr);
+      g.qt = w + L.dzt;
+      g.ldqt = L.ldt;
+      g.fb = fb;
+    }
     RLK_TRY(launch_fwd_gemm(b->dtype, g, true, s), "fwd_gemm");
 
     TokenParams tp = {};
@@ -648,6 +667,16 @@ rlk_status_t rlk_pg_loss_fwd_bwd(const rlk_batch_t* b, const void* hidden, const
     tp.ref_logp = p->kl_coef > 0.0f ? p->ref_logp : nullptr;
     tp.kl_coef = p->kl_coef;
     tp.token_adv = p->token_adv;
+    if (ref_layout) {
+      tp.zr = F(L.zr);
+      tp.st = F(L.st);
+      tp.fb = fb;
+      tp.q = w + L.q;
+      tp.qt = w + L.dzt;
+      tp.ldq = L.ldq;
+      tp.ldqt = L.ldt;
+      tp.V = b->V;
+    }
     RLK_TRY(launch_combine(tp, s), "combine");
 
     DzParams dp = {};
@@ -668,7 +697,11 @@ rlk_status_t rlk_pg_loss_fwd_bwd(const rlk_batch_t* b, const void* hidden, const
     dp.et = tp.et;
     dp.ytgt = tp.ytgt;
     dp.has_ent = p->entropy_coef != 0.0f;
+    dp.fb = ref_layout ? fb : nullptr;
+    dp.ndz = &hdr->n_dz_chunks;
     RLK_TRY(launch_dz(b->dtype, dp, s), "dz");
+    if (ref_layout)
+      RLK_TRY(launch_hidden_t(w + L.hc, b->d, F(L.st), fb, hdr, c0, L.Mc, w + L.ht, L.ldt, s), "hidden_t");
 
     GemmArgs h = {};
     h.A = w + L.q;
@@ -684,6 +717,10 @@ rlk_status_t rlk_pg_loss_fwd_bwd(const rlk_batch_t* b, const void* hidden, const
     h.out = dhidden;
     h.idx = I(L.idx);
     h.ldo = b->d;
+    if (ref_layout) {
+      h.rs = F(L.st);
+      h.rs_off = fb;
+    }
     set_split(h, L.sk_dh, w + L.part);
     RLK_TRY(launch_dh_gemm(b->dtype, h, s), "dh_gemm");
 
@@ -730,6 +767,7 @@ rlk_status_t rlk_pg_loss_fwd_bwd(const rlk_batch_t* b, const void* hidden, const
   lp.token_adv = p->token_adv;
   lp.loss = loss;
   lp.stats = stats;
+  lp.nchunks = L.nchunks;
   RLK_TRY(launch_loss(lp, s, 0), "loss");
   RLK_TRY(launch_zero_fill(b->dtype, reinterpret_cast<const uint8_t*>(w + L.keep), N, b->d, dhidden, logp_out,
                            entropy_out, nullptr, s),

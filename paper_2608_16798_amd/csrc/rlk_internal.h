@@ -27,6 +27,16 @@ constexpr int kChunkAlign = 256; // chunk_rows granularity
 constexpr int kKAlign = 64;      // K padding of the chunk buffers (bf16 elements per stage)
 constexpr int kGemmSliceBytes = 128;  // bytes of K per GEMM pipeline slice and row
 
+// Token-reference layout of the stored probabilities (bf16 fwd+bwd without an entropy term):
+// q_tj = exp(z_tj - ref_t) with ref_t = the target logit z_{t,y_t}, the same for every vocabulary
+// tile of the token, so dL/dz = diag(s) q up to the target entry (s_t = -g_t exp(ref_t - lse_t)).
+// A tile whose maximum exceeds ref_t by more than kRefSpan stores against max - kRefSpan instead
+// and marks the chunk, whose dz is then formed explicitly; kRefQMax and kRefSMin bound the patched
+// target entry and |s_t| for the same purpose (no bf16 overflow, no fp32 denormal scales).
+constexpr float kRefSpan = 40.0f;
+constexpr float kRefQMax = 1e30f;
+constexpr float kRefSMin = 1e-30f;
+
 // Split-K plan of a gradient GEMM with at most mmax x n outputs and kbytes of K per row: with
 // fewer than 128 output tiles the K range is split over s workgroups per tile (each at least 4
 // slices), so the launch still fills the GPU; the fp32 partials go to a workspace buffer of
@@ -80,6 +90,8 @@ enum KernelKind {
   KK_GAE,
   KK_VALUE_LOSS,
   KK_VALUE_HEAD,
+  KK_TARGET_LOGIT,
+  KK_HIDDEN_T,
   KK_COUNT_KINDS
 };
 
@@ -89,7 +101,9 @@ struct WsHeader {
   int32_t n_eff;     // number of trained tokens
   int32_t n_groups;  // Q
   int32_t n_valid;   // non-excluded rollouts
-  int32_t pad[60];
+  int32_t ref_fallback;  // current chunk: 1 = its token-reference layout does not hold, dz explicit
+  int32_t n_dz_chunks;   // chunks whose dz was formed explicitly
+  int32_t pad[58];
 };
 
 // Byte offsets of the workspace segments (all 256-aligned).
@@ -110,6 +124,7 @@ struct WsLayout {
   size_t q = 0;                    // T [Mc][ldq]
   size_t dzt = 0;                  // T [Vp][ldt]
   size_t wt = 0;                   // T [d][ldw]
+  size_t zr = 0, st = 0;           // float [Mc]: reference logit and dz row scale per chunk row
   size_t part = 0;                 // float split-K partials of the dhidden / dW GEMMs (0 = none)
   SplitK sk_dh = {1, 1}, sk_dw = {1, 1};
   int64_t Mc = 0;                  // chunk rows
@@ -138,6 +153,13 @@ hipError_t launch_transpose_w(int dtype, const void* W, void* WT, int V, int64_t
                               hipStream_t s);
 hipError_t launch_gather(int dtype, const void* hidden, int d, const int32_t* idx, const WsHeader* hdr,
                          int64_t c0, int64_t Mc, void* hc, void* ht, int64_t ldt, bool want_ht, hipStream_t s);
+// bf16: zr[t] = (hc[t] . W[ytgt[c0 + t]]) / tau for the chunk's rows; clears *fb.
+hipError_t launch_target_logit(const void* hc, int d, const void* W, const int32_t* ytgt, const WsHeader* hdr,
+                               int64_t c0, int64_t Mc, int V, float inv_tau, float* zr, int32_t* fb,
+                               hipStream_t s);
+// bf16: HT[j][t] = hc[t][j] * (*fb ? 1 : st[t]) (zero columns t >= rows, up to the K pad).
+hipError_t launch_hidden_t(const void* hc, int d, const float* st, const int32_t* fb, const WsHeader* hdr,
+                           int64_t c0, int64_t Mc, void* ht, int64_t ldt, hipStream_t s);
 
 struct TokenParams {
   const WsHeader* hdr;
@@ -161,6 +183,14 @@ struct TokenParams {
   float kl_coef;
   const float* token_adv;      // per-token advantages (NULL = group advantages)
   float inv_tau;               // 1 / temperature: dL/d(W h) = dL/dz / tau
+  // token-reference layout (bf16; zr = NULL: off): reference logits zr [Mc]; out: the target entries of
+  // q [Mc][ldq] and q^T [Vp][ldqt], the row scales st [Mc] and *fb |= 1 where the bounds fail
+  const float* zr;
+  float* st;
+  int32_t* fb;
+  void *q, *qt;
+  int64_t ldq, ldqt;
+  int V;
 };
 hipError_t launch_combine(const TokenParams& p, hipStream_t s);
 
@@ -174,6 +204,8 @@ struct DzParams {
   const float *pm, *lse, *logp, *ent, *gt, *et;
   const int32_t* ytgt;
   int has_ent;
+  const int32_t* fb;   // non-NULL: run only when *fb != 0 (token-reference layout not usable)
+  int32_t* ndz;        // counts the chunks that ran (may be NULL)
 };
 hipError_t launch_dz(int dtype, const DzParams& p, hipStream_t s);
 
@@ -193,6 +225,7 @@ struct LossParams {
   const float* token_adv;
   float* loss;
   rlk_pg_stats_t* stats;
+  int32_t nchunks;
 };
 hipError_t launch_loss(const LossParams& p, hipStream_t s, int prof_kind_first);
 
@@ -232,10 +265,18 @@ struct GemmArgs {
   int64_t ldq;
   int V;
   float inv_tau;         // logits z = acc / tau
+  // token-reference layout (bf16 forward; zr = NULL: each tile stores against its own maximum):
+  // reference logits zr [Mc], q^T [Vp][ldqt] written beside q, *fb = 1 where a tile clamps
+  const float* zr;
+  void* qt;
+  int64_t ldqt;
+  int32_t* fb;
   // dhidden epilogue
   void* out;
   const int32_t* idx;
   int64_t ldo;
+  const float* rs;       // row scales [Mc] applied unless *rs_off != 0 (NULL: none)
+  const int32_t* rs_off;
   // dW epilogue
   float* dw;
   int accumulate;

@@ -178,6 +178,7 @@ def compare_full(inst, gpu, ref, params, tag=""):
     m["kl_mean_err"] = abs(st["kl_mean"] - ref["stats"]["kl_mean"]) / max(1.0, abs(ref["stats"]["kl_mean"]))
     m["tis_mean_err"] = abs(st["tis_mean"] - ref["stats"]["tis_mean"])
     m["flags"] = gpu["flags"]
+    m["dz_chunks"] = f"{st['n_dz_chunks']}/{st['n_chunks']}"
     log(f"[{tag}] {cfg.name}: " + ", ".join(f"{k}={v:.3g}" if isinstance(v, float) else f"{k}={v}"
                                             for k, v in m.items()))
     tl = TOL_LOGP[cfg.dtype]
@@ -188,4 +189,14 @@ def compare_full(inst, gpu, ref, params, tag=""):
     assert m["dh_rel"] <= TOL_GRAD and m["dW_rel"] <= TOL_GRAD
     assert m["stats_ok"]
     assert m["kl_mean_err"] <= 1e-3 and m["tis_mean_err"] <= 1e-4
+    # the explicit dz pass runs for every chunk unless the token-reference layout applies (bf16
+    # without an entropy term), where it runs only for the chunks flagged on the device
+    assert st["n_chunks"] >= 1 and 0 <= st["n_dz_chunks"] <= st["n_chunks"]
+    if not ref_layout(cfg, params):
+        assert st["n_dz_chunks"] == st["n_chunks"]
     return m
+
+
+def ref_layout(cfg, params):
+    """Whether a fwd+bwd call of this configuration stores q against the target logits."""
+    return cfg.dtype == "bf16" and params.entropy_coef == 0.0

@@ -10,7 +10,7 @@ import numpy as np
 import pytest
 
 from gpu_common import (TOL_GRAD, TOL_LOSS, aux_logps, loss_error, TOL_LOGP, O, WL, build_instance, compare_full, ensure_library, log,
-                        params_for, rel_fro, rlk, run_gpu, run_oracle, to_host)
+                        params_for, ref_layout, rel_fro, rlk, run_gpu, run_oracle, to_host)
 
 pytestmark = pytest.mark.gpu
 
@@ -338,6 +338,10 @@ def test_full_size_sampled_rows(name):
     log(f"full-size {name} N={st.N}")
     gpu = run_gpu(inst, p)
     assert gpu["flags"] == 0
+    sg = gpu["stats"]
+    log(f"  explicit dz in {sg['n_dz_chunks']} of {sg['n_chunks']} chunks")
+    # every chunk of these batches keeps the token-reference layout when it applies
+    assert sg["n_dz_chunks"] == (0 if ref_layout(cfg, p) else sg["n_chunks"])
     idx, tr, npol = O.compact(st.mask, st.cu_seqlens, st.group_ids)
     ga = O.group_advantage(st.rewards, st.group_ids, p.adv_eps)
     assert gpu["stats"]["n_policy_tokens"] == idx.shape[0] and gpu["stats"]["n_groups"] == ga["n_groups"]
@@ -397,16 +401,18 @@ def test_full_size_sampled_rows(name):
 # Ragged shapes: hidden sizes that are not a multiple of the 64-element K slice (the forward GEMM's
 # K tail, the dhidden/dW GEMMs' ragged N), vocabularies that are not a multiple of the 256-row
 # tile (and smaller than one tile), token counts that leave partial token tiles.
-RAGGED = [("tiny_fp32", dict(d=264, V=1000)), ("tiny_fp32", dict(d=40, V=100)),
-          ("small_bf16", dict(d=136, V=777)), ("small_bf16", dict(d=520, V=4099))]
+# The bf16 shapes run with and without the entropy term (without it, the token-reference layout).
+RAGGED = [("tiny_fp32", dict(d=264, V=1000), 0.02), ("tiny_fp32", dict(d=40, V=100), 0.02),
+          ("small_bf16", dict(d=136, V=777), 0.02), ("small_bf16", dict(d=520, V=4099), 0.02),
+          ("small_bf16", dict(d=136, V=777), 0.0), ("small_bf16", dict(d=520, V=4099), 0.0)]
 
 
-@pytest.mark.parametrize("name,kw", RAGGED)
-def test_pg_loss_parity_ragged_shapes(name, kw):
+@pytest.mark.parametrize("name,kw,ent", RAGGED)
+def test_pg_loss_parity_ragged_shapes(name, kw, ent):
     base = WL.get_config(name) if name == "tiny_fp32" else WL.scaled_config(name)
     cfg = base.with_(name=f"{base.name}_d{kw['d']}_V{kw['V']}", w_std=1.0 / np.sqrt(kw["d"]), **kw)
     inst = build_instance(cfg)
-    p = params_for(cfg, entropy_coef=0.02, chunk_rows=256)
+    p = params_for(cfg, entropy_coef=ent, chunk_rows=256)
     log(f"pg_loss ragged {cfg.name} N={inst['st'].N}")
     compare_full(inst, run_gpu(inst, p), run_oracle(inst, p), p, tag="ragged")
     # the log-prob forward alone on the same shapes
@@ -472,13 +478,14 @@ def test_pg_loss_maximum_rollout_count():
 
 
 # Sampling temperature: logits z = W h / tau in the forward and the gradients.
-@pytest.mark.parametrize("name,scaled,tau", [("tiny_fp32", False, 0.7), ("small_bf16", True, 1.3)])
-def test_pg_loss_temperature_parity(name, scaled, tau):
+@pytest.mark.parametrize("name,scaled,tau,ent", [("tiny_fp32", False, 0.7, 0.02), ("small_bf16", True, 1.3, 0.02),
+                                                  ("small_bf16", True, 0.6, 0.0)])
+def test_pg_loss_temperature_parity(name, scaled, tau, ent):
     import torch
 
     cfg = WL.scaled_config(name) if scaled else WL.get_config(name)
     inst = build_instance(cfg)
-    p = params_for(cfg, entropy_coef=0.02, chunk_rows=256 if scaled else 0)
+    p = params_for(cfg, entropy_coef=ent, chunk_rows=256 if scaled else 0)
     log(f"pg_loss temperature {tau} {cfg.name} N={inst['st'].N}")
     compare_full(inst, run_gpu(inst, p, temperature=tau), run_oracle(inst, p, temperature=tau), p, tag=f"tau={tau}")
     logp, ent, lse, ws = rlk.logprob_fwd(inst["h"], inst["W"], inst["targets"], inst["mask"], inst["cu"],
@@ -489,3 +496,42 @@ def test_pg_loss_temperature_parity(name, scaled, tau):
     rl, rp, rH = O.token_logprob(to_host(inst["h"])[idx], to_host(inst["W"]), inst["st"].targets[idx], temperature=tau)
     tol = TOL_LOGP[cfg.dtype]
     assert np.abs(logp.cpu().numpy()[idx] - rp).max() <= tol and np.abs(ent.cpu().numpy()[idx] - rH).max() <= tol
+
+
+# Token-reference layout (bf16 without an entropy term): the stored probabilities are taken against
+# each token's target logit, dz = diag(s) q is applied inside the GEMMs and no chunk needs the
+# explicit dz pass.  One token whose hidden row is scaled by 64 (exact in bf16) and whose target is
+# its smallest logit (log-prob near -700, far beyond the 40-nat span) sends exactly its own chunk to
+# the explicit pass; its old log-prob is set next to the new one so that its gradient is not zero.
+def test_token_reference_layout_and_its_fallback():
+    import dataclasses
+
+    import torch
+
+    cfg = WL.scaled_config("qwen8b_bf16")
+    inst = build_instance(cfg)
+    p = params_for(cfg, chunk_rows=256)
+    gpu = run_gpu(inst, p)
+    compare_full(inst, gpu, run_oracle(inst, p), p, tag="ref layout")
+    assert gpu["stats"]["n_chunks"] >= 3 and gpu["stats"]["n_dz_chunks"] == 0
+
+    st = inst["st"]
+    idx = O.compact(st.mask, st.cu_seqlens, st.group_ids)[0]
+    t = int(idx[len(idx) // 2])
+    h = inst["h"].clone()
+    h[t] *= 64
+    W64 = to_host(inst["W"]).astype(np.float64)
+    y = int(np.argmin(W64 @ to_host(h[t]).astype(np.float64)))
+    targets = st.targets.copy()
+    targets[t] = y
+    lp = float(O.token_logprob(to_host(h[t:t + 1]), to_host(inst["W"]), np.array([y]))[1][0])
+    assert lp < -100.0, lp
+    old = inst["old_host"].copy()
+    old[t] = lp + 0.05
+    inst2 = dict(inst, st=dataclasses.replace(st, targets=targets), h=h,
+                 targets=torch.as_tensor(targets, dtype=torch.int32, device="cuda"),
+                 old=torch.as_tensor(old, dtype=torch.float32, device="cuda"), old_host=old)
+    log(f"fallback token {t} (chunk {int(np.searchsorted(idx, t)) // 256}): target {y}, log-prob {lp:.1f}")
+    gpu2 = run_gpu(inst2, p)
+    compare_full(inst2, gpu2, run_oracle(inst2, p), p, tag="ref fallback")
+    assert gpu2["stats"]["n_dz_chunks"] == 1
