@@ -135,6 +135,29 @@ int64_t plan_chunk_rows(int64_t B, int64_t cap, int64_t d, int64_t Vp) {
   return best;
 }
 
+// The dW GEMM's V x d outputs form whole waves of 256 tiles plus a partial last wave, whose time is
+// that of a whole one (K = the chunk's tokens, the longest tiles of the step at large chunks).  The
+// tile rows of that wave go to a second launch split over K into as many parts as fit one wave
+// (partials reduced in split order), when that is at least 2 parts.
+void plan_dw_tail(int64_t V, int64_t d, int64_t kbytes, WsLayout& L) {
+  L.dw_m0 = 0;
+  L.sk_dwt = {1, 1};
+  if (L.sk_dw.s > 1) return;
+  const int64_t tm = (V + kTile - 1) / kTile, tn = (d + kTile - 1) / kTile, tail = tm * tn % 256;
+  if (tail == 0) return;
+  const int64_t r = (tail + tn - 1) / tn;  // tile rows holding the partial wave
+  const int64_t s = 256 / (r * tn);
+  const int64_t nk = (kbytes + kGemmSliceBytes - 1) / kGemmSliceBytes;
+  if (r >= tm || s < 2 || nk < 2) return;
+  const int64_t ks = (nk + s - 1) / s;
+  L.sk_dwt = {(int)((nk + ks - 1) / ks), (int)ks};
+  if (L.sk_dwt.s < 2) {
+    L.sk_dwt = {1, 1};
+    return;
+  }
+  L.dw_m0 = (tm - r) * kTile;
+}
+
 rlk_status_t layout(const rlk_batch_t* b, bool bwd, int64_t chunk_rows, WsLayout& L) {
   const int64_t esz = b->dtype == RLK_DTYPE_BF16 ? 2 : 4;
   const int64_t N = b->N, R = b->R, d = b->d, V = b->V;
@@ -149,7 +172,7 @@ rlk_status_t layout(const rlk_batch_t* b, bool bwd, int64_t chunk_rows, WsLayout
   if (Mc == 0) {
     int64_t per_row = (int64_t)L.nvt * 12 + d * esz;
     if (bwd) per_row += d * esz + 2 * L.Vp * esz;
-    const int64_t budget = bwd ? ((int64_t)24 << 30) : ((int64_t)4 << 30);
+    const int64_t budget = bwd ? ((int64_t)40 << 30) : ((int64_t)4 << 30);
     Mc = budget / per_row / kChunkAlign * kChunkAlign;
     if (Mc > 65536) Mc = 65536;
     if (Mc < kChunkAlign) Mc = kChunkAlign;
@@ -205,7 +228,9 @@ rlk_status_t layout(const rlk_batch_t* b, bool bwd, int64_t chunk_rows, WsLayout
     // split-K partials of the dhidden and dW GEMMs (used one after the other)
     L.sk_dh = splitk_plan(Mc, d, L.Vp * esz);
     L.sk_dw = splitk_plan(V, d, Mc * esz);
-    const size_t pb = std::max(splitk_bytes(Mc, d, L.sk_dh), splitk_bytes(V, d, L.sk_dw));
+    plan_dw_tail(V, d, Mc * esz, L);
+    const size_t pb = std::max({splitk_bytes(Mc, d, L.sk_dh), splitk_bytes(V, d, L.sk_dw),
+                                splitk_bytes(V - L.dw_m0, d, L.sk_dwt)});
     if (pb > 0) L.part = a.take(pb);
   }
   // The GEMMs address each 256-row operand panel with 32-bit buffer offsets and mark rows past a
@@ -593,6 +618,7 @@ rlk_status_t rlk_pg_loss_fwd_bwd(const rlk_batch_t* b, const void* hidden, const
   // the scaled transpose of the gathered rows apply s, and the explicit dz pass runs only for chunks
   // flagged on the device (a token whose target lies too far below its largest logits).
   const bool ref_layout = b->dtype == RLK_DTYPE_BF16 && p->entropy_coef == 0.0f;
+  const size_t esz = b->dtype == RLK_DTYPE_BF16 ? 2 : 4;
   int32_t* fb = &hdr->ref_fallback;
   for (int c = 0; c < L.nchunks; ++c) {
     const int64_t c0 = (int64_t)c * L.Mc;
@@ -739,7 +765,19 @@ rlk_status_t rlk_pg_loss_fwd_bwd(const rlk_batch_t* b, const void* hidden, const
     k.ldo = b->d;
     k.accumulate = p->accumulate_dW;
     set_split(k, L.sk_dw, w + L.part);
-    RLK_TRY(launch_dw_gemm(b->dtype, k, s), "dw_gemm");
+    if (L.dw_m0 > 0) {
+      // the tile rows of the partial last wave, split over K
+      GemmArgs t = k;
+      t.A = w + L.dzt + (size_t)L.dw_m0 * L.ldt * esz;
+      t.M = b->V - (int)L.dw_m0;
+      t.dw = dW + L.dw_m0 * b->d;
+      set_split(t, L.sk_dwt, w + L.part);
+      k.M = (int)L.dw_m0;
+      RLK_TRY(launch_dw_gemm(b->dtype, k, s), "dw_gemm");
+      RLK_TRY(launch_dw_gemm(b->dtype, t, s), "dw_gemm tail");
+    } else {
+      RLK_TRY(launch_dw_gemm(b->dtype, k, s), "dw_gemm");
+    }
   }
 
   LossParams lp = {};

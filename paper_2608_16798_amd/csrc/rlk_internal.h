@@ -127,6 +127,10 @@ struct WsLayout {
   size_t zr = 0, st = 0;           // float [Mc]: reference logit and dz row scale per chunk row
   size_t part = 0;                 // float split-K partials of the dhidden / dW GEMMs (0 = none)
   SplitK sk_dh = {1, 1}, sk_dw = {1, 1};
+  // dW launch of a large shape (sk_dw none): output tiles from row dw_m0 on (the partial last wave of
+  // 256 tiles, whole tile rows) go to a second launch split over K by sk_dwt; dw_m0 = 0: one launch
+  int64_t dw_m0 = 0;
+  SplitK sk_dwt = {1, 1};
   int64_t Mc = 0;                  // chunk rows
   int64_t Vp = 0;                  // vocabulary padded to 256
   // Row strides (elements) of the chunk buffers read by the gradient GEMMs: padded by 64 when the
