@@ -276,7 +276,8 @@ def read_occupancy(workload: str, digest: str):
     return flop, occ
 
 
-HBM_KERNELS = ("k_dz", "k_gather", "k_target_logit", "k_hidden_t", "k_transpose_w", "k_zero_fill", "k_combine")
+HBM_KERNELS = ("k_dz", "k_dz_flagged", "k_gather", "k_target_logit", "k_hidden_t", "k_transpose_w", "k_zero_fill",
+               "k_combine")
 
 
 def hbm_kernel_summary(fetch_csv, write_csv, workload, copy_mib, cmd_fetch, cmd_write):
@@ -298,11 +299,12 @@ def hbm_kernel_summary(fetch_csv, write_csv, workload, copy_mib, cmd_fetch, cmd_
     # flagged, the gather writes h_c only, and the s-scaled h_c^T comes after the combine
     ref = cfg.dtype == "bf16" and cfg.entropy_coef == 0.0
     hrow = n_eff * cfg.d * esz
-    alg = {"k_dz": 0 if ref else 3 * n_eff * vp * esz, "k_gather": (2 if ref else 3) * hrow,
+    alg = {"k_dz": 3 * n_eff * vp * esz, "k_dz_flagged": 0, "k_gather": (2 if ref else 3) * hrow,
            "k_target_logit": 2 * hrow, "k_hidden_t": 2 * hrow,
            "k_transpose_w": (cfg.V + vp) * cfg.d * esz, "k_zero_fill": (st.N - n_eff) * (cfg.d * esz + 8),
            "k_combine": n_eff * (12 * (vp // 256) + 40)}
-    what = {"k_dz": "none: no chunk flagged (token-reference layout)" if ref else "read q, write dz and dz^T",
+    what = {"k_dz": "read q, write dz and dz^T",
+            "k_dz_flagged": "dz of flagged chunks only; none expected here, every block exits at once",
             "k_gather": "read h rows, write h_c" + ("" if ref else " and h_c^T"),
             "k_target_logit": "read h_c rows and the target rows of W",
             "k_hidden_t": "read h_c, write the row-scaled h_c^T",
