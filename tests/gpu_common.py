@@ -200,3 +200,28 @@ def compare_full(inst, gpu, ref, params, tag=""):
 def ref_layout(cfg, params):
     """Whether a fwd+bwd call of this configuration stores q against the target logits."""
     return cfg.dtype == "bf16" and params.entropy_coef == 0.0
+
+
+def with_far_target(inst, t):
+    """The instance with token t's hidden row scaled by 64 (exact in bf16) and its target set to its
+    smallest logit, so that its log-prob is far below -40 (about -700 at the qwen8b shape), and its
+    old log-prob set next to the new one so that its gradient is not zero.  Returns (instance, logp)."""
+    import dataclasses
+
+    import torch
+
+    st = inst["st"]
+    h = inst["h"].clone()
+    h[t] *= 64
+    W64 = to_host(inst["W"]).astype(np.float64)
+    y = int(np.argmin(W64 @ to_host(h[t]).astype(np.float64)))
+    targets = st.targets.copy()
+    targets[t] = y
+    lp = float(O.token_logprob(to_host(h[t:t + 1]), to_host(inst["W"]), np.array([y]))[1][0])
+    old = inst["old_host"].copy()
+    old[t] = lp + 0.05
+    dev = h.device
+    out = dict(inst, st=dataclasses.replace(st, targets=targets), h=h,
+               targets=torch.as_tensor(targets, dtype=torch.int32, device=dev),
+               old=torch.as_tensor(old, dtype=torch.float32, device=dev), old_host=old)
+    return out, lp

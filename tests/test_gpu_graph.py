@@ -11,7 +11,7 @@ from __future__ import annotations
 
 import pytest
 
-from gpu_common import WL, build_instance, ensure_library, log, params_for
+from gpu_common import O, WL, build_instance, ensure_library, log, params_for, with_far_target
 
 pytestmark = pytest.mark.gpu
 
@@ -63,21 +63,31 @@ def _assert_same(got, ref, tag):
         assert same, f"{tag}: {k} differs from the eager call"
 
 
-@pytest.mark.parametrize("name,chunk_rows", [("small_bf16", 0), ("large_bf16", 256)])
-def test_pg_loss_graph_replay(name, chunk_rows):
+# small_bf16 (no entropy term): the token-reference layout, no chunk flagged; large_bf16: the dz pass in
+# every chunk; qwen8b_bf16 with one far target: the layout with exactly one flagged chunk, whose flag
+# each replay must clear and set again.
+@pytest.mark.parametrize("name,chunk_rows,far", [("small_bf16", 0, False), ("large_bf16", 256, False),
+                                                 ("qwen8b_bf16", 256, True)])
+def test_pg_loss_graph_replay(name, chunk_rows, far):
     import torch
 
     import paper_2608_16798_amd as rlk
 
     cfg = WL.scaled_config(name)
     inst = build_instance(cfg)
+    if far:
+        st = inst["st"]
+        idx = O.compact(st.mask, st.cu_seqlens, st.group_ids)[0]
+        inst, _ = with_far_target(inst, int(idx[len(idx) // 2]))
     p = params_for(cfg, chunk_rows=chunk_rows)
-    log(f"graph replay {cfg.name} N={inst['h'].shape[0]} chunk_rows={chunk_rows}")
+    log(f"graph replay {cfg.name} N={inst['h'].shape[0]} chunk_rows={chunk_rows} far target {far}")
 
     eager = _buffers(inst, p)
     _call(inst, p, eager)
     torch.cuda.synchronize()
     ref = _snapshot(eager)
+    if far:
+        assert ref["stats"]["n_dz_chunks"] == 1
 
     buf = _buffers(inst, p)
     side = torch.cuda.Stream()
