@@ -158,15 +158,17 @@ def test_pg_loss_parity(name, scaled, chunk):
     compare_full(inst, gpu, ref, p, tag="seq")
 
 
-@pytest.mark.parametrize("name,scaled,agg", [("tiny_fp32", False, rlk.AGG_SEQ), ("small_bf16", True, rlk.AGG_SEQ),
-                                             ("qwen8b_bf16", True, rlk.AGG_TOKEN)])
-def test_pg_loss_tis_and_kl_parity(name, scaled, agg):
+@pytest.mark.parametrize("name,scaled,agg,ent", [("tiny_fp32", False, rlk.AGG_SEQ, 0.01),
+                                                 ("small_bf16", True, rlk.AGG_SEQ, 0.01),
+                                                 ("qwen8b_bf16", True, rlk.AGG_TOKEN, 0.01),
+                                                 ("qwen8b_bf16", True, rlk.AGG_SEQ, 0.0)])
+def test_pg_loss_tis_and_kl_parity(name, scaled, agg, ent):
     """Truncated importance sampling (Sec. 3.2.4) and the KL term (Sec. 2.3.2), both on, the cap
-    binding on part of the tokens."""
+    binding on part of the tokens; without the entropy term through the token-reference layout."""
     cfg = WL.scaled_config(name) if scaled else WL.get_config(name)
     inst = build_instance(cfg)
     aux = aux_logps(inst)
-    p = params_for(cfg, agg=agg, tis_cap=1.1, kl_coef=0.05, entropy_coef=0.01, chunk_rows=256 if scaled else 0)
+    p = params_for(cfg, agg=agg, tis_cap=1.1, kl_coef=0.05, entropy_coef=ent, chunk_rows=256 if scaled else 0)
     log(f"pg_loss tis+kl {cfg.name} N={inst['st'].N}")
     gpu = run_gpu(inst, p, aux=aux)
     ref = run_oracle(inst, p, aux=aux)
@@ -452,12 +454,12 @@ def test_split_k_accumulates_into_preset_dw():
 # Degenerate vocabulary: with V = 1 every policy token has log-prob 0, entropy 0 and a zero
 # logit gradient, so dhidden and dW are 0 (one valid row in a 256-row tile); the GPU reaches
 # them up to the fp32 rounding of exp2 / log at z = max.
-@pytest.mark.parametrize("name,d", [("tiny_fp32", 64), ("small_bf16", 128)])
-def test_pg_loss_single_entry_vocabulary(name, d):
+@pytest.mark.parametrize("name,d,ent", [("tiny_fp32", 64, 0.02), ("small_bf16", 128, 0.02), ("small_bf16", 128, 0.0)])
+def test_pg_loss_single_entry_vocabulary(name, d, ent):
     base = WL.get_config(name) if name == "tiny_fp32" else WL.scaled_config(name)
     cfg = base.with_(name=f"{base.name}_V1", d=d, V=1, w_std=1.0 / np.sqrt(d))
     inst = build_instance(cfg)
-    p = params_for(cfg, entropy_coef=0.02)
+    p = params_for(cfg, entropy_coef=ent)
     gpu = run_gpu(inst, p)
     compare_full(inst, gpu, run_oracle(inst, p), p, tag="V=1")
     assert float(gpu["logp"].abs().max()) <= 1e-6 and float(gpu["ent"].abs().max()) <= 1e-6
