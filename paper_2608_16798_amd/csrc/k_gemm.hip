@@ -4,6 +4,8 @@
 //   forward : A = W [V, d],          B = gathered hidden [tokens, d]   -> online log-softmax
 //   dhidden : A = dz [tokens, Vp],   B = W^T [d, Vp]                   -> scatter to dh[idx]
 //   dW      : A = dz^T [Vp, tokens], B = hidden^T [d, tokens]          -> fp32 dW (+)=
+// In the token-reference layout (dz = diag(s) q) the gradient GEMMs read the forward's q and q^T
+// as A, the dhidden epilogue scales its rows by s and the dW GEMM's B is (diag(s) hidden)^T.
 //
 // Tile geometry (gfx950): a 256 x 256 output tile per workgroup of WAVES_M x WAVES_N = 2 x 4
 // wavefronts (two per SIMD), each owning a 128 x 64 block of 32 x 32 v_mfma_f32_32x32x16_bf16
@@ -589,8 +591,8 @@ __global__ void __launch_bounds__(NT) k_gemm(GemmArgs a) {
     }
     if constexpr (STORE_Q && sizeof(T) == 2) {
       // phase 3: coalesced copy of the staged bf16 tile to q[n][v0 .. v0 + 255].  q is read once,
-      // by the dz kernel after this launch: non-temporal stores keep it from displacing the
-      // operand panels that later tiles of this launch re-read from the caches.
+      // by the dz kernel or the dhidden GEMM after this launch: non-temporal stores keep it from
+      // displacing the operand panels that later tiles of this launch re-read from the caches.
       const int chunk = tid & 31;
 #pragma unroll 4
       for (int it = 0; it < kTile * 32 / NT; ++it) {
