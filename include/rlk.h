@@ -110,7 +110,9 @@ typedef struct {
   double norm_override; /* > 0: replaces Q (SEQ) or the policy-token count (TOKEN) so that
                            micro-batched calls add up to the one-call gradient */
   int64_t chunk_rows;   /* policy tokens per backward chunk, multiple of 256, at most
-                           RLK_MAX_CHUNK_ROWS; 0 = auto */
+                           RLK_MAX_CHUNK_ROWS; 0 = auto: the largest multiple of 256, at most
+                           65,536, whose chunk buffers fit 40 GiB (4 GiB for rlk_logprob_fwd),
+                           then, with max_policy_tokens, the fewest chunks covering the bound */
   /* Token-level truncated importance sampling (Sec. 3.2.4): with rollout_logp (device [N] f32,
    * the inference engine's log-prob of each sampled token) the loss of token t is scaled by
    * w_t = min(exp(old_logp[t] - rollout_logp[t]), tis_cap), held constant in the gradient.
