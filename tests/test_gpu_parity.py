@@ -522,3 +522,10 @@ def test_token_reference_layout_and_its_fallback():
     gpu2 = run_gpu(inst2, p)
     compare_full(inst2, gpu2, run_oracle(inst2, p), p, tag="ref fallback")
     assert gpu2["stats"]["n_dz_chunks"] == 1
+
+    # the scale bound: a normaliser of 1e24 puts g_t near 1e-26 and the row scales s_t = -g_t p_y
+    # below 1e-30 (fp32 denormals once multiplied), so those chunks form dz explicitly as well
+    p3 = params_for(cfg, chunk_rows=256, norm_override=1e24)
+    gpu3 = run_gpu(inst, p3)
+    compare_full(inst, gpu3, run_oracle(inst, p3), p3, tag="ref tiny scales")
+    assert gpu3["stats"]["n_dz_chunks"] >= 1
