@@ -322,13 +322,16 @@ N_SAMPLED_ROWS = 1024
 N_DW_ROWS = 64
 
 
-@pytest.mark.parametrize("name", ["small_bf16", "qwen8b_bf16", "long_bf16", "large_bf16"])
-def test_full_size_sampled_rows(name):
+@pytest.mark.parametrize("name,far", [("small_bf16", False), ("qwen8b_bf16", False), ("long_bf16", False),
+                                      ("large_bf16", False), ("qwen8b_bf16", True)])
+def test_full_size_sampled_rows(name, far):
     """Full-size batch in the configuration the benchmark times: integer outputs bit-exact;
     per-token log-prob / entropy and dhidden rows exact on 1,024 seeded sampled rows (a row
     depends only on itself and per-rollout scalars); the loss re-aggregated in fp64 from the
     GPU's per-token log-probs and entropies; 64 seeded dW rows from the GPU's per-token values
-    (each is a sum over every policy token); the zero column sum of dW."""
+    (each is a sum over every policy token); the zero column sum of dW.  With far, one policy token
+    in the middle of the batch gets a target about 700 nats below its largest logit, so its chunk
+    (one of the full-size chunks) forms dz explicitly; that token joins the sampled rows."""
     import time
 
     import torch
@@ -337,14 +340,23 @@ def test_full_size_sampled_rows(name):
     inst = build_instance(cfg)
     st = inst["st"]
     p = params_for(cfg)
+    idx, tr, npol = O.compact(st.mask, st.cu_seqlens, st.group_ids)
+    far_pos = None
+    if far:
+        far_pos = idx.shape[0] // 2 + 12345
+        inst, lp_far = with_far_target(inst, int(idx[far_pos]))
+        st = inst["st"]
+        log(f"  far target at policy token {far_pos} (row {int(idx[far_pos])}), log-prob {lp_far:.1f}")
     log(f"full-size {name} N={st.N}")
     gpu = run_gpu(inst, p)
     assert gpu["flags"] == 0
     sg = gpu["stats"]
     log(f"  explicit dz in {sg['n_dz_chunks']} of {sg['n_chunks']} chunks")
-    # every chunk of these batches keeps the token-reference layout when it applies
-    assert sg["n_dz_chunks"] == (0 if ref_layout(cfg, p) else sg["n_chunks"])
-    idx, tr, npol = O.compact(st.mask, st.cu_seqlens, st.group_ids)
+    # every chunk of these batches keeps the token-reference layout when it applies (with far: all but one)
+    if far:
+        assert sg["n_dz_chunks"] == 1
+    else:
+        assert sg["n_dz_chunks"] == (0 if ref_layout(cfg, p) else sg["n_chunks"])
     ga = O.group_advantage(st.rewards, st.group_ids, p.adv_eps)
     assert gpu["stats"]["n_policy_tokens"] == idx.shape[0] and gpu["stats"]["n_groups"] == ga["n_groups"]
     omega = O.token_weights(tr, npol, ga["group_index"], ga["G"], ga["n_groups"], p.agg)
@@ -355,6 +367,8 @@ def test_full_size_sampled_rows(name):
 
     # sampled rows: forward and dhidden
     pick = np.sort(WL.sample_policy_rows(np.arange(idx.shape[0]), N_SAMPLED_ROWS, seed=cfg.seed + 7))
+    if far_pos is not None:
+        pick = np.unique(np.append(pick, far_pos))
     rows = idx[pick]
     rows_t = torch.as_tensor(rows, device="cuda")
     ref = O.sampled_rows(to_host(inst["h"][rows_t]), W_host, st.targets[rows], old_pol[pick], adv_tok[pick],
