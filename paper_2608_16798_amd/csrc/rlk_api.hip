@@ -158,6 +158,38 @@ void plan_dw_tail(int64_t V, int64_t d, int64_t kbytes, WsLayout& L) {
   L.dw_m0 = (tm - r) * kTile;
 }
 
+// The dhidden GEMM of a chunk known to hold at most `rows` trained tokens (the caller's bound): its
+// tile rows x d output tiles end in a partial wave of 256 tiles that costs a whole wave of the longest
+// tiles of the step (K = Vp).  Those tile rows go to a second launch split over K into s parts, which
+// takes ceil(tail tiles x s / 256) waves of 1/s of the work; s (2-16, each part at least 4 slices) is
+// the smallest within 0.02 waves of the quickest, and only a saving of a tenth of a wave is taken.
+struct DhTail {
+  int64_t m0 = 0;  // first tile row of the tail (rows); 0 = one launch
+  SplitK sk = {1, 1};
+  int64_t rows = 0;  // rows of the tail launch (whole tiles)
+};
+DhTail plan_dh_tail(int64_t rows, int64_t d, int64_t kbytes) {
+  DhTail t;
+  const int64_t tc = (rows + kTile - 1) / kTile, tn = (d + kTile - 1) / kTile, tail = tc * tn % 256;
+  const int64_t nk = (kbytes + kGemmSliceBytes - 1) / kGemmSliceBytes;
+  if (tail == 0 || tc * tn < 256) return t;
+  const int64_t r = (tail + tn - 1) / tn;
+  if (r >= tc) return t;
+  auto waves = [&](int64_t s) { return (double)((r * tn * s + 255) / 256) / (double)s; };
+  double best = 1.0;
+  for (int64_t s = 2; s <= 16 && nk / s >= 4; ++s) best = std::min(best, waves(s));
+  if (best > 0.9) return t;
+  int64_t sel = 2;
+  while (waves(sel) > best + 0.02) ++sel;
+  const int64_t ks = (nk + sel - 1) / sel;
+  const SplitK sk = {(int)((nk + ks - 1) / ks), (int)ks};
+  if (sk.s < 2) return t;
+  t.sk = sk;
+  t.m0 = (tc - r) * kTile;
+  t.rows = r * kTile;
+  return t;
+}
+
 rlk_status_t layout(const rlk_batch_t* b, bool bwd, int64_t chunk_rows, WsLayout& L) {
   const int64_t esz = b->dtype == RLK_DTYPE_BF16 ? 2 : 4;
   const int64_t N = b->N, R = b->R, d = b->d, V = b->V;
@@ -183,6 +215,7 @@ rlk_status_t layout(const rlk_batch_t* b, bool bwd, int64_t chunk_rows, WsLayout
   const int64_t B = b->max_policy_tokens > 0 ? std::min<int64_t>(b->max_policy_tokens, N) : N;
   if (b->max_policy_tokens > 0 && B > 0) Mc = plan_chunk_rows(B, Mc, d, L.Vp);
   L.Mc = Mc;
+  L.rows_bound = B;
   L.nchunks = (int32_t)((B + Mc - 1) / Mc);
   if (bwd && L.nchunks < 1) L.nchunks = 1;
 
@@ -229,8 +262,13 @@ rlk_status_t layout(const rlk_batch_t* b, bool bwd, int64_t chunk_rows, WsLayout
     L.sk_dh = splitk_plan(Mc, d, L.Vp * esz);
     L.sk_dw = splitk_plan(V, d, Mc * esz);
     plan_dw_tail(V, d, Mc * esz, L);
-    const size_t pb = std::max({splitk_bytes(Mc, d, L.sk_dh), splitk_bytes(V, d, L.sk_dw),
-                                splitk_bytes(V - L.dw_m0, d, L.sk_dwt)});
+    size_t pb = std::max({splitk_bytes(Mc, d, L.sk_dh), splitk_bytes(V, d, L.sk_dw),
+                          splitk_bytes(V - L.dw_m0, d, L.sk_dwt)});
+    if (L.sk_dh.s == 1 && b->max_policy_tokens > 0)
+      for (int64_t c0 = 0; c0 < B; c0 += Mc) {
+        const DhTail t = plan_dh_tail(std::min(Mc, B - c0), d, L.Vp * esz);
+        if (t.m0 > 0) pb = std::max(pb, splitk_bytes(t.rows, d, t.sk));
+      }
     if (pb > 0) L.part = a.take(pb);
   }
   // The GEMMs address each 256-row operand panel with 32-bit buffer offsets and mark rows past a
@@ -748,7 +786,26 @@ rlk_status_t rlk_pg_loss_fwd_bwd(const rlk_batch_t* b, const void* hidden, const
       h.rs_off = fb;
     }
     set_split(h, L.sk_dh, w + L.part);
-    RLK_TRY(launch_dh_gemm(b->dtype, h, s), "dh_gemm");
+    const DhTail dt = L.sk_dh.s == 1 && b->max_policy_tokens > 0
+                          ? plan_dh_tail(std::min(L.Mc, L.rows_bound - c0), b->d, L.Vp * esz)
+                          : DhTail{};
+    if (dt.m0 > 0) {
+      // the tile rows of the partial last wave, split over K: the same GEMM on the chunk rows from
+      // c0 + m0 (the kernels read the trained-token count relative to c0)
+      GemmArgs t = h;
+      t.A = w + L.q + (size_t)dt.m0 * L.ldq * esz;
+      t.M = (int)dt.rows;
+      t.c0 = c0 + dt.m0;
+      t.Mc = dt.rows;
+      if (t.rs) t.rs += dt.m0;
+      set_split(t, dt.sk, w + L.part);
+      h.M = (int)dt.m0;
+      h.Mc = dt.m0;
+      RLK_TRY(launch_dh_gemm(b->dtype, h, s), "dh_gemm");
+      RLK_TRY(launch_dh_gemm(b->dtype, t, s), "dh_gemm tail");
+    } else {
+      RLK_TRY(launch_dh_gemm(b->dtype, h, s), "dh_gemm");
+    }
 
     GemmArgs k = {};
     k.A = w + L.dzt;

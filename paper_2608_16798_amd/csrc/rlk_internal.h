@@ -131,6 +131,7 @@ struct WsLayout {
   // 256 tiles, whole tile rows) go to a second launch split over K by sk_dwt; dw_m0 = 0: one launch
   int64_t dw_m0 = 0;
   SplitK sk_dwt = {1, 1};
+  int64_t rows_bound = 0;          // trained tokens the chunk loop covers (N, or the caller's bound)
   int64_t Mc = 0;                  // chunk rows
   int64_t Vp = 0;                  // vocabulary padded to 256
   // Row strides (elements) of the chunk buffers read by the gradient GEMMs: padded by 64 when the

@@ -347,8 +347,11 @@ def test_full_size_sampled_rows(name, far):
         inst, lp_far = with_far_target(inst, int(idx[far_pos]))
         st = inst["st"]
         log(f"  far target at policy token {far_pos} (row {int(idx[far_pos])}), log-prob {lp_far:.1f}")
-    log(f"full-size {name} N={st.N}")
-    gpu = run_gpu(inst, p)
+    # the benchmark passes the host-known count of trained tokens as the bound (without far: chunks sized
+    # by it, and dhidden tile rows of a partial last wave split over K; with far: chunks over all N)
+    bound = 0 if far else int(idx.shape[0])
+    log(f"full-size {name} N={st.N} max_policy_tokens={bound}")
+    gpu = run_gpu(inst, p, max_policy_tokens=bound)
     assert gpu["flags"] == 0
     sg = gpu["stats"]
     log(f"  explicit dz in {sg['n_dz_chunks']} of {sg['n_chunks']} chunks")
@@ -543,3 +546,23 @@ def test_token_reference_layout_and_its_fallback():
     gpu3 = run_gpu(inst, p3)
     compare_full(inst, gpu3, run_oracle(inst, p3), p3, tag="ref tiny scales")
     assert gpu3["stats"]["n_dz_chunks"] >= 1
+
+
+# The dhidden GEMM's partial last wave of 256 tiles, split over K in a second launch (chunk rows known
+# from the bound): d = 1024 (4 tile columns), V = 4096 and 20,610 trained tokens in one chunk give 81
+# tile rows, 324 tiles and a 68-tile tail (17 tile rows), split 7 ways.  Parity with and without the
+# bound (without it the chunk is one launch).
+def test_dhidden_tail_split_over_k():
+    base = WL.scaled_config("small_bf16")
+    cfg = base.with_(name="small_bf16_d1024_V4096", groups=4, rollouts_per_group=8, len_min=1024, len_max=1024,
+                     d=1024, V=4096, w_std=1.0 / 32.0)
+    inst = build_instance(cfg)
+    st = inst["st"]
+    n_eff = int(O.compact(st.mask, st.cu_seqlens, st.group_ids)[0].shape[0])
+    assert 256 * 64 < n_eff <= 65536 and (n_eff + 255) // 256 * 4 % 256 > 0
+    p = params_for(cfg)
+    ref = run_oracle(inst, p)
+    for bound in (n_eff, 0):
+        log(f"dhidden tail split: N_eff={n_eff} bound={bound}")
+        gpu = run_gpu(inst, p, max_policy_tokens=bound)
+        compare_full(inst, gpu, ref, p, tag=f"dh tail bound={bound}")
