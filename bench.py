@@ -497,6 +497,8 @@ def main():
     ap.add_argument("--no-policy-bound", action="store_true",
                     help="do not pass the host-known count of policy tokens (max_policy_tokens = 0: the chunk loop "
                          "covers all N rows)")
+    ap.add_argument("--no-grad-hint", action="store_true",
+                    help="do not pass the host count of tokens in groups of unequal rewards (grad_tokens = 0)")
     ap.add_argument("--logprob-only", action="store_true",
                     help="time rlk_logprob_fwd alone (the pi_old forward pass, 2 N_eff V d FLOP per call)")
     ap.add_argument("--no-kernel-events", action="store_true",
@@ -561,6 +563,8 @@ def main():
     params = rlk.make_params(eps_low=cfg.eps_low, eps_high=cfg.eps_high, entropy_coef=cfg.entropy_coef,
                              chunk_rows=args.chunk_rows)
     bound = 0 if args.no_policy_bound else host_policy_tokens(st, exclusion=not args.logprob_only)
+    if bound and not args.logprob_only and not args.no_grad_hint:
+        params.grad_tokens = rlk.grad_token_hint(st.mask, st.cu_seqlens, st.rewards, st.group_ids)
     batch = rlk.make_batch(inp["h"], inp["W"], inp["cu"], max_policy_tokens=bound)
     ws = rlk.alloc_workspace(rlk.workspace_size(batch, None if args.logprob_only else params), dev)
     ws_adv = rlk.alloc_workspace(rlk.advantage_workspace_size(R), dev)
@@ -643,8 +647,13 @@ def main():
     step_ms = [ev[i].elapsed_time(ev[i + 1]) for i in range(args.steps)]
     ms_per_step = float(np.median(step_ms))
     value = n_eff / (ms_per_step / 1e3)
-    n_mm = 1 if args.logprob_only else 3
-    alg_flops = 2.0 * n_mm * n_eff * cfg.V * cfg.d
+    # Algorithmic MFMA work: 2 V d per trained token for the forward, and 2 V d for each gradient GEMM
+    # per token that carries a surrogate gradient (the device's count: without an entropy term, a KL
+    # term or per-token advantages, the tokens of zero-advantage rollouts skip the backward GEMMs).
+    n_grad = n_eff
+    if not args.logprob_only:
+        n_grad = int(rlk.stats_from_tensor(stats)["n_grad_tokens"])
+    alg_flops = 2.0 * (n_eff if args.logprob_only else n_eff + 2 * n_grad) * cfg.V * cfg.d
     peak = PEAK_BF16 if cfg.dtype == "bf16" else PEAK_FP32_MFMA
     mfma_frac = alg_flops / (ms_per_step / 1e3) / peak
     log(f"[bench] {ms_per_step:.2f} ms/step (median; mean {np.mean(step_ms):.2f}, wall {(t1 - t0) * 1e3 / args.steps:.2f}), "
@@ -658,7 +667,7 @@ def main():
         dom = max(GEMM_KINDS, key=lambda k: kern.get(k, (0.0, 1))[0])
         ms, cnt = kern[dom]
         avg_ms = ms / cnt
-        flops_per_launch = 2.0 * n_eff * cfg.V * cfg.d * args.steps / cnt
+        flops_per_launch = 2.0 * (n_eff if dom == "fwd_lse_gemm" else n_grad) * cfg.V * cfg.d * args.steps / cnt
         achieved = flops_per_launch / (avg_ms / 1e3) / 1e12
         digest = kernel_source_digest()
         traffic = None if args.logprob_only else read_traffic(dom, cfg.name, digest, cnt // args.steps)
@@ -691,14 +700,20 @@ def main():
         "metric": metric, "value": round(value, 1), "unit": "policy tokens/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": round(ms_per_step, 3), "higher_is_better": True, "scaling": "weak",
         "vs_baseline": None, "dtype": cfg.dtype, "data": "synthetic",
-        "config": dict(WL.configs.describe(cfg, N), N_eff=n_eff, chunk_rows=args.chunk_rows or "auto",
-                       max_policy_tokens=bound, **({"graph": True} if args.graph else {}),
+        "config": dict(WL.configs.describe(cfg, N), N_eff=n_eff,
+                       **({} if args.logprob_only else {"N_grad": n_grad}), chunk_rows=args.chunk_rows or "auto",
+                       max_policy_tokens=bound, **({} if args.logprob_only else {"grad_tokens": params.grad_tokens}),
+                       **({"graph": True} if args.graph else {}),
                        **({"call": "rlk_logprob_fwd"} if args.logprob_only else {})),
         "timing": {"ms_per_step_median": round(ms_per_step, 3), "ms_per_step_mean": round(float(np.mean(step_ms)), 3),
                    "ms_per_step_min": round(float(np.min(step_ms)), 3), "ms_per_step_max": round(float(np.max(step_ms)), 3),
                    "ms_wall_per_step": round((t1 - t0) * 1e3 / args.steps, 3),
                    "per_kernel_events": use_events, "dz_chunks": dz_chunks},
         "mfma_pct_of_peak": round(100 * mfma_frac, 2),
+        "flop_accounting": {"alg_mfma_flop_per_step": alg_flops, "forward_tokens": n_eff,
+                            "backward_tokens": n_grad,
+                            "pct_of_peak_at_6_N_eff_V_d": round(100 * (2.0 * (1 if args.logprob_only else 3) * n_eff
+                                                                       * cfg.V * cfg.d) / (ms_per_step / 1e3) / peak, 2)},
         "executed_mfma_pct": executed["pct_of_peak"] if executed else None, "executed_mfma": executed,
         "roofline": roofline, "cpu_baseline": cpu, "kernels": per_kernel,
     }

@@ -48,7 +48,7 @@
 extern "C" {
 #endif
 
-#define RLK_VERSION 6
+#define RLK_VERSION 7
 
 typedef int32_t rlk_status_t;
 enum {
@@ -129,6 +129,12 @@ typedef struct {
    * the group advantages; NULL = group advantages (GRPO).  Rewards and group ids still define
    * exclusion and the SEQ aggregation. */
   const float* token_adv;
+  /* Optional host-known count of the trained tokens whose rollout advantage is not 0 (the tokens
+   * that go through the backward when the loss has no entropy term, KL term or per-token
+   * advantages; see rlk_pg_loss_fwd_bwd), with max_policy_tokens > 0: the chunk loop then puts a
+   * chunk boundary at that count, so the backward runs on well-filled chunks.  0 = unknown.  It only
+   * plans the chunks: any value gives the same results.  Must be >= 0. */
+  int64_t grad_tokens;
 } rlk_pg_params_t;
 
 typedef struct {
@@ -145,6 +151,9 @@ typedef struct {
   int32_t n_chunks;       /* chunk iterations of the call */
   int32_t n_dz_chunks;    /* chunks whose logit gradient dz was formed explicitly (see
                            * rlk_pg_loss_fwd_bwd); the others applied dz = diag(s) q in the GEMMs */
+  int64_t n_grad_tokens;  /* policy tokens that went through the backward GEMMs: N_eff, less the
+                           * tokens of rollouts whose advantage is exactly 0 when the loss has no
+                           * other term (see rlk_pg_loss_fwd_bwd) */
 } rlk_pg_stats_t;
 
 /* Workspace bytes needed by rlk_logprob_fwd (p == NULL) or by rlk_pg_loss_fwd_bwd (p
@@ -216,7 +225,11 @@ rlk_status_t rlk_group_advantage_noalloc(int32_t R, const float* rewards, const 
  * against each token's target logit, which makes dz = diag(s) q with q the stored values (target
  * entry adjusted), so the dhidden and dW GEMMs apply the row scale s and dz is never written; a
  * chunk holding a token with a target far below its largest logits (log-prob below about -40)
- * forms dz explicitly instead, with the same result.  stats->n_dz_chunks counts those chunks. */
+ * forms dz explicitly instead, with the same result.  stats->n_dz_chunks counts those chunks.
+ * Without an entropy term, a KL term or per-token advantages, the surrogate gradient of a rollout
+ * whose advantage is exactly 0 (every rollout of an all-equal group) is exactly 0: its tokens get
+ * the forward (log-prob, entropy, loss, stats) but skip the backward GEMMs, and their dhidden rows
+ * are written as 0; stats->n_grad_tokens counts the tokens that went through the backward. */
 rlk_status_t rlk_pg_loss_fwd_bwd(const rlk_batch_t* b, const void* hidden, const void* W,
                                  const int32_t* targets, const uint8_t* mask,
                                  const float* old_logp, const float* rewards,

@@ -39,7 +39,7 @@ class PgParams(ctypes.Structure):
                 ("entropy_coef", ctypes.c_float), ("agg", ctypes.c_int32), ("accumulate_dW", ctypes.c_int32),
                 ("norm_override", ctypes.c_double), ("chunk_rows", ctypes.c_int64),
                 ("rollout_logp", ctypes.c_void_p), ("ref_logp", ctypes.c_void_p), ("tis_cap", ctypes.c_float),
-                ("kl_coef", ctypes.c_float), ("token_adv", ctypes.c_void_p)]
+                ("kl_coef", ctypes.c_float), ("token_adv", ctypes.c_void_p), ("grad_tokens", ctypes.c_int64)]
 
 
 class PgStats(ctypes.Structure):
@@ -47,7 +47,7 @@ class PgStats(ctypes.Structure):
                 ("clip_frac", ctypes.c_float), ("ratio_mean", ctypes.c_float), ("n_groups", ctypes.c_int32),
                 ("n_valid_rollouts", ctypes.c_int32), ("n_policy_tokens", ctypes.c_int64),
                 ("kl_mean", ctypes.c_float), ("tis_mean", ctypes.c_float), ("n_chunks", ctypes.c_int32),
-                ("n_dz_chunks", ctypes.c_int32)]
+                ("n_dz_chunks", ctypes.c_int32), ("n_grad_tokens", ctypes.c_int64)]
 
 
 class Calls(ctypes.Structure):
@@ -215,9 +215,10 @@ def make_batch(hidden, W, cu_seqlens, temperature: float = 1.0, max_policy_token
 
 
 def make_params(eps_low=0.2, eps_high=None, adv_eps=1e-6, entropy_coef=0.0, agg=AGG_SEQ, accumulate_dW=False,
-                norm_override=0.0, chunk_rows=0, tis_cap=0.0, kl_coef=0.0) -> PgParams:
+                norm_override=0.0, chunk_rows=0, tis_cap=0.0, kl_coef=0.0, grad_tokens=0) -> PgParams:
     """Loss parameters; the rollout / reference log-prob arrays of truncated importance sampling
-    and of the KL term are passed to pg_loss_fwd_bwd."""
+    and of the KL term are passed to pg_loss_fwd_bwd.  grad_tokens is the optional chunk-planning
+    hint (see grad_token_hint)."""
     p = PgParams()
     p.eps_low = eps_low
     p.eps_high = eps_low if eps_high is None else eps_high
@@ -229,7 +230,34 @@ def make_params(eps_low=0.2, eps_high=None, adv_eps=1e-6, entropy_coef=0.0, agg=
     p.chunk_rows = int(chunk_rows)
     p.tis_cap = float(tis_cap)
     p.kl_coef = float(kl_coef)
+    p.grad_tokens = int(grad_tokens)
     return p
+
+
+def grad_token_hint(mask, cu_seqlens, rewards, group_ids) -> int:
+    """Host count for PgParams.grad_tokens: trained tokens (mask = 1) of the rollouts with a group id
+    >= 0 whose group's rewards are not all equal.  A group of equal rewards has the advantage 0 for
+    every member (Sec. 2.3.1), so without an entropy term, KL term or per-token advantages its tokens
+    carry no gradient and the call leaves them out of the backward.  It is a planning hint only: a
+    rollout whose advantage comes out 0 in a mixed group is still counted, which any value tolerates."""
+    import numpy as np
+
+    cu = np.asarray(cu_seqlens, dtype=np.int64)
+    gid = np.asarray(group_ids, dtype=np.int64)
+    rw = np.asarray(rewards, dtype=np.float64)
+    lens = np.diff(cu)
+    live = gid >= 0
+    mixed = np.zeros(len(gid), dtype=bool)
+    if live.any():
+        groups, inv = np.unique(gid[live], return_inverse=True)
+        lo = np.full(len(groups), np.inf)
+        hi = np.full(len(groups), -np.inf)
+        np.minimum.at(lo, inv, rw[live])
+        np.maximum.at(hi, inv, rw[live])
+        mixed[live] = (hi > lo)[inv]
+    keep = np.repeat(mixed, lens)
+    m = np.asarray(mask)[:keep.shape[0]].astype(bool)
+    return int((m & keep).sum())
 
 
 def workspace_size(batch: Batch, params: Optional[PgParams] = None) -> int:

@@ -218,7 +218,9 @@ __global__ void __launch_bounds__(NT) k_gemm(GemmArgs a) {
   __shared__ __attribute__((aligned(16))) char smem[DEEP_B ? LDS_DEEP_B : LDS_B];
 
   int M = a.M, N = a.N, K = a.K;
-  int64_t rc = (int64_t)a.hdr->n_eff - a.c0;
+  // rows of the chunk: every trained token for the forward, those with a surrogate gradient for the
+  // gradient GEMMs
+  int64_t rc = (int64_t)(EPI == EPI_FWD ? a.hdr->n_eff : a.hdr->n_grad) - a.c0;
   rc = rc < 0 ? 0 : (rc > a.Mc ? a.Mc : rc);
   if (EPI == EPI_FWD) N = (int)rc;
   if (EPI == EPI_DH) M = (int)rc;
@@ -479,6 +481,13 @@ __global__ void __launch_bounds__(NT) k_gemm(GemmArgs a) {
     const int v0 = tile_m * kTile;
     const int V = a.V;
     const bool full_v = v0 + kTile <= V;
+    // q and q^T are read only for the tokens with a surrogate gradient (the first n_grad of the
+    // list): the stores stop there (q^T writes zero columns up to the K pad)
+    int ng = N;
+    if constexpr (STORE_Q) {
+      const int64_t g = (int64_t)a.hdr->n_grad - a.c0;
+      ng = g < 0 ? 0 : (g < N ? (int)g : N);
+    }
     float* red_m = reinterpret_cast<float*>(smem + RED_OFF);  // [WAVES_M][256]
     float* red_s = red_m + WAVES_M * kTile;                    // [WAVES_M][256]
     float* red_u = red_s + WAVES_M * kTile;                    // [WAVES_M][256]
@@ -553,7 +562,7 @@ __global__ void __launch_bounds__(NT) k_gemm(GemmArgs a) {
               *reinterpret_cast<u32x2*>(sQ + cl * QROW + rl0 * 2) = pk;
             } else {
               const int n = tile_n * kTile + cl;
-              if (n < N) {
+              if (n < ng) {
                 float* qp = reinterpret_cast<float*>(a.q) + (int64_t)n * a.ldq + v0 + rl0;
 #pragma unroll
                 for (int i = 0; i < 4; ++i) qp[i] = ev[i];
@@ -598,7 +607,7 @@ __global__ void __launch_bounds__(NT) k_gemm(GemmArgs a) {
       for (int it = 0; it < kTile * 32 / NT; ++it) {
         const int cl = (tid >> 5) + (NT / 32) * it;
         const int n = tile_n * kTile + cl;
-        if (n < N) {
+        if (n < ng) {
           const u32x4 v = *reinterpret_cast<const u32x4*>(sQ + cl * QROW + chunk * 16);
           char* dst = reinterpret_cast<char*>(a.q) + ((int64_t)n * a.ldq + v0) * 2 + chunk * 16;
           __builtin_nontemporal_store(v, reinterpret_cast<u32x4*>(dst));
@@ -606,20 +615,22 @@ __global__ void __launch_bounds__(NT) k_gemm(GemmArgs a) {
       }
       if (a.qt) {
         // phase 4: the same tile transposed into q^T[v0 .. v0 + 255][tokens of the tile], the dW
-        // GEMM's operand (columns of tokens >= N as zero).  Each lane transposes an 8 x 8 square in
+        // GEMM's operand (columns of tokens >= n_grad as zero, up to the K pad).  Each lane transposes an 8 x 8 square in
         // registers: wavefront w covers 64 x 64 blocks w and w + 8, lane (a8, b8) the vocabulary
         // rows 8 a8 .. + 7 and tokens 8 b8 .. + 7 of a block.  The LDS reads of 8 consecutive lanes
         // span one 128-byte row segment (conflict free); each store writes 8 full 128-byte lines.
         const int a8 = lane & 7, b8 = lane >> 3;
+        const int ngpad = (ng + kKAlign - 1) / kKAlign * kKAlign;
 #pragma unroll
         for (int it = 0; it < kTile * kTile / 4096 / NWAVE; ++it) {
           const int blk = wid + NWAVE * it;
           const int rl0 = (blk & 3) * 64 + a8 * 8, cl0 = (blk >> 2) * 64 + b8 * 8;
           const int n0 = tile_n * kTile + cl0;
+          if (n0 >= ngpad) continue;
           u32x4 in[8];
 #pragma unroll
           for (int j = 0; j < 8; ++j)
-            in[j] = n0 + j < N ? *reinterpret_cast<const u32x4*>(sQ + (cl0 + j) * QROW + rl0 * 2) : u32x4{0, 0, 0, 0};
+            in[j] = n0 + j < ng ? *reinterpret_cast<const u32x4*>(sQ + (cl0 + j) * QROW + rl0 * 2) : u32x4{0, 0, 0, 0};
 #pragma unroll
           for (int k = 0; k < 8; ++k) {
             u32x4 o;
@@ -681,7 +692,7 @@ __global__ void __launch_bounds__(NT) k_gemm(GemmArgs a) {
 // scatter or the dW overwrite / accumulate.  Rows and the empty-chunk rule follow the GEMM.
 template <typename T, int EPI>
 __global__ void __launch_bounds__(256) k_splitk_reduce(GemmArgs a) {
-  int64_t rc = (int64_t)a.hdr->n_eff - a.c0;
+  int64_t rc = (int64_t)a.hdr->n_grad - a.c0;
   rc = rc < 0 ? 0 : (rc > a.Mc ? a.Mc : rc);
   int M = a.M;
   if (EPI == EPI_DH) M = (int)rc;

@@ -4,6 +4,10 @@
 // tokens are optimised) inside rollouts that are not excluded (Sec. 3.4: sandbox
 // failures leave advantage estimation and policy optimisation), in ascending order.  Every
 // later GEMM operand is gathered through this list, so masked tokens cost no MFMA work.
+// Optionally (zero_grad: the caller's loss has no term but the advantage-weighted surrogate) the
+// tokens of rollouts whose advantage is exactly 0 (an all-equal group, Sec. 2.3.2) go after all
+// others, in their own ascending run: their surrogate gradient is exactly 0, so the backward
+// covers only the first n_grad rows of the list while the forward covers all n_eff.
 // The per-rollout count of kept tokens is the normaliser of the per-rollout token mean
 // (masked GRPO objective, Sec. 2.3.2; shared-prefix tokens counted once, Sec. 3.2.3).
 //
@@ -61,6 +65,7 @@ __global__ void __launch_bounds__(kThreads) k_begin(WsHeader* hdr, const int32_t
   if (threadIdx.x == 0) {
     hdr->status = err;
     hdr->n_eff = 0;
+    hdr->n_grad = 0;
     hdr->n_groups = 0;
     hdr->n_valid = 0;
     hdr->ref_fallback = 0;
@@ -74,101 +79,125 @@ __device__ inline bool keep_token(const uint8_t* mask, const int32_t* gid, int r
   return k;
 }
 
+// keep[t]: 0 = not trained, 1 = trained, 2 = trained with an exactly zero surrogate gradient (its
+// rollout's advantage is 0 and zero_adv is given).  blkcnt[b] counts the 1s of block b and
+// blkcnt[nblk + b] its 2s, so one exclusive scan over both halves places every 2 after every 1.
 __global__ void __launch_bounds__(kThreads)
-k_count(const uint8_t* mask, const int32_t* cu, const int32_t* gid, int R, int64_t N, uint8_t* keep,
-        int32_t* blkcnt) {
-  __shared__ int partial[kThreads / 64];
+k_count(const uint8_t* mask, const int32_t* cu, const int32_t* gid, const float* zero_adv, int R, int64_t N,
+        uint8_t* keep, int32_t* blkcnt, int nblk) {
+  __shared__ int partial[2][kThreads / 64];
   const int64_t t0 = (int64_t)blockIdx.x * kScanTile + (int64_t)threadIdx.x * kPerThread;
-  int cnt = 0;
+  int cnt1 = 0, cnt2 = 0;
   if (t0 < N) {
     int r = rollout_of(cu, R, t0);
     for (int i = 0; i < kPerThread; ++i) {
       int64_t t = t0 + i;
       if (t >= N) break;
       while (r < R - 1 && (int64_t)cu[r + 1] <= t) ++r;
-      bool k = keep_token(mask, gid, r, t);
-      keep[t] = k ? 1 : 0;
-      cnt += k ? 1 : 0;
+      const bool k = keep_token(mask, gid, r, t);
+      const bool zg = k && zero_adv && zero_adv[r] == 0.0f;
+      keep[t] = !k ? 0 : (zg ? 2 : 1);
+      cnt1 += (k && !zg) ? 1 : 0;
+      cnt2 += zg ? 1 : 0;
     }
   }
-  cnt = wave_sum(cnt);
+  cnt1 = wave_sum(cnt1);
+  cnt2 = wave_sum(cnt2);
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  if (lane == 0) partial[w] = cnt;
+  if (lane == 0) {
+    partial[0][w] = cnt1;
+    partial[1][w] = cnt2;
+  }
   __syncthreads();
-  if (threadIdx.x == 0) {
+  if (threadIdx.x < 2) {
     int s = 0;
-    for (int i = 0; i < kThreads / 64; ++i) s += partial[i];
-    blkcnt[blockIdx.x] = s;
+    for (int i = 0; i < kThreads / 64; ++i) s += partial[threadIdx.x][i];
+    blkcnt[threadIdx.x * nblk + blockIdx.x] = s;
   }
 }
 
-// Exclusive scan of the per-block counts; n_eff = the total.  With a caller bound on the trained
-// tokens (max_policy > 0) a larger total is flagged and n_eff clamped to the bound, so every later
-// kernel stays within the chunk loop the host sized for it.
-__global__ void __launch_bounds__(1024) k_scan(const int32_t* blkcnt, int32_t* blkoff, int nblk, int32_t max_policy,
-                                               WsHeader* hdr) {
+// Exclusive scan of the per-block counts (both halves: nblk2 = 2 nblk); n_eff = the total, n_grad =
+// the offset of the second half (the tokens with a gradient).  With a caller bound on the trained
+// tokens (max_policy > 0) a larger total is flagged and both counts clamped to the bound, so every
+// later kernel stays within the chunk loop the host sized for it.
+__global__ void __launch_bounds__(1024) k_scan(const int32_t* blkcnt, int32_t* blkoff, int nblk2, int nblk,
+                                               int32_t max_policy, WsHeader* hdr) {
   __shared__ int wsum[16];
-  __shared__ int carry_s;
+  __shared__ int carry_s, ngrad_s;
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   if (threadIdx.x == 0) carry_s = 0;
   __syncthreads();
-  for (int base = 0; base < nblk; base += 1024) {
+  for (int base = 0; base < nblk2; base += 1024) {
     int i = base + threadIdx.x;
-    int v = i < nblk ? blkcnt[i] : 0;
+    int v = i < nblk2 ? blkcnt[i] : 0;
     int inc = wave_inclusive_scan(v, lane);
     if (lane == 63) wsum[w] = inc;
     __syncthreads();
     int woff = 0;
     for (int j = 0; j < w; ++j) woff += wsum[j];
     int carry = carry_s;
-    if (i < nblk) blkoff[i] = carry + woff + inc - v;
+    if (i < nblk2) blkoff[i] = carry + woff + inc - v;
+    if (i == nblk) ngrad_s = carry + woff + inc - v;
     __syncthreads();
     if (threadIdx.x == 1023) carry_s = carry + woff + inc;
     __syncthreads();
   }
   if (threadIdx.x == 0) {
-    int n = carry_s;
+    int n = carry_s, g = ngrad_s;
     if (max_policy > 0 && n > max_policy) {
       atomicOr(&hdr->status, RLK_DERR_POLICY_BOUND);
       n = max_policy;
+      g = g < n ? g : n;
     }
     hdr->n_eff = n;
+    hdr->n_grad = g;
   }
 }
 
 __global__ void __launch_bounds__(kThreads)
-k_write_idx(const uint8_t* keep, const int32_t* cu, int R, int64_t N, const int32_t* blkoff,
+k_write_idx(const uint8_t* keep, const int32_t* cu, int R, int64_t N, const int32_t* blkoff, int nblk,
             const int32_t* targets, int V, int32_t* idx, int32_t* tokr, int32_t* ytgt, float* zy,
             WsHeader* hdr) {
-  __shared__ int wsum[kThreads / 64];
+  __shared__ int wsum[2][kThreads / 64];
   const int64_t t0 = (int64_t)blockIdx.x * kScanTile + (int64_t)threadIdx.x * kPerThread;
-  int cnt = 0;
+  int cnt1 = 0, cnt2 = 0;
   for (int i = 0; i < kPerThread; ++i) {
     int64_t t = t0 + i;
-    if (t < N) cnt += keep[t];
+    if (t < N) {
+      cnt1 += keep[t] == 1;
+      cnt2 += keep[t] == 2;
+    }
   }
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  int inc = wave_inclusive_scan(cnt, lane);
-  if (lane == 63) wsum[w] = inc;
+  const int inc1 = wave_inclusive_scan(cnt1, lane), inc2 = wave_inclusive_scan(cnt2, lane);
+  if (lane == 63) {
+    wsum[0][w] = inc1;
+    wsum[1][w] = inc2;
+  }
   __syncthreads();
-  int off = blkoff[blockIdx.x];
-  for (int j = 0; j < w; ++j) off += wsum[j];
-  off += inc - cnt;
-  if (cnt == 0) return;
+  int off1 = blkoff[blockIdx.x], off2 = blkoff[nblk + blockIdx.x];
+  for (int j = 0; j < w; ++j) {
+    off1 += wsum[0][j];
+    off2 += wsum[1][j];
+  }
+  off1 += inc1 - cnt1;
+  off2 += inc2 - cnt2;
+  if (cnt1 + cnt2 == 0) return;
   int r = rollout_of(cu, R, t0);
   int bad = 0;
   for (int i = 0; i < kPerThread; ++i) {
     int64_t t = t0 + i;
     if (t >= N) break;
     while (r < R - 1 && (int64_t)cu[r + 1] <= t) ++r;
-    if (keep[t]) {
+    const uint8_t k = keep[t];
+    if (k) {
       const int y = targets ? targets[t] : 0;
       if (y < 0 || y >= V) bad = 1;
+      const int off = k == 1 ? off1++ : off2++;
       idx[off] = (int32_t)t;
       tokr[off] = r;
       ytgt[off] = y;
       zy[off] = 0.0f;
-      ++off;
     }
   }
   if (bad) atomicOr(&hdr->status, RLK_DERR_TARGET);
@@ -184,16 +213,20 @@ __device__ inline int lower_bound_i32(const int32_t* a, int n, int64_t key) {
 }
 
 __global__ void __launch_bounds__(kThreads)
-k_rollout_offsets(const int32_t* cu, int R, int64_t N, const int32_t* idx, const WsHeader* hdr,
-                  int32_t* rstart, int32_t* rnpol) {
+k_rollout_offsets(const int32_t* cu, int R, int64_t N, const int32_t* idx, const float* zero_adv,
+                  const WsHeader* hdr, int32_t* rstart, int32_t* rnpol) {
   const int r = blockIdx.x * blockDim.x + threadIdx.x;
   if (r >= R) return;
-  const int n = hdr->n_eff;
+  // the rollout's tokens form one ascending run inside its part of the list: [0, n_grad) or, for a
+  // rollout of zero advantage, [n_grad, n_eff)
+  const int ng = hdr->n_grad, n = hdr->n_eff;
+  const bool second = zero_adv && zero_adv[r] == 0.0f;
+  const int lo = second ? ng : 0, hi = second ? n : ng;
   int64_t a = cu[r], b = cu[r + 1];
   a = a < 0 ? 0 : (a > N ? N : a);
   b = b < a ? a : (b > N ? N : b);
-  int s = lower_bound_i32(idx, n, a);
-  int e = lower_bound_i32(idx, n, b);
+  int s = lo + lower_bound_i32(idx + lo, hi - lo, a);
+  int e = lo + lower_bound_i32(idx + lo, hi - lo, b);
   rstart[r] = s;
   rnpol[r] = e - s;
 }
@@ -347,21 +380,21 @@ hipError_t launch_begin(int32_t* status_hdr, const int32_t* cu, int R, int64_t N
 }
 
 hipError_t launch_compact(const uint8_t* mask, const int32_t* cu, const int32_t* gid, int R, int64_t N,
-                          const int32_t* targets, int V, int32_t max_policy, char* ws, const WsLayout& L,
-                          hipStream_t s) {
+                          const int32_t* targets, int V, int32_t max_policy, const float* zero_adv, char* ws,
+                          const WsLayout& L, hipStream_t s) {
   WsHeader* hdr = reinterpret_cast<WsHeader*>(ws + L.hdr);
   uint8_t* keep = reinterpret_cast<uint8_t*>(ws + L.keep);
   int32_t* blkcnt = reinterpret_cast<int32_t*>(ws + L.blkcnt);
   int32_t* blkoff = reinterpret_cast<int32_t*>(ws + L.blkoff);
   if (N > 0) {
     prof_mark(KK_COUNT, true, s);
-    k_count<<<L.nblk, kThreads, 0, s>>>(mask, cu, gid, R, N, keep, blkcnt);
+    k_count<<<L.nblk, kThreads, 0, s>>>(mask, cu, gid, zero_adv, R, N, keep, blkcnt, L.nblk);
     prof_mark(KK_COUNT, false, s);
     prof_mark(KK_SCAN, true, s);
-    k_scan<<<1, 1024, 0, s>>>(blkcnt, blkoff, L.nblk, max_policy, hdr);
+    k_scan<<<1, 1024, 0, s>>>(blkcnt, blkoff, 2 * L.nblk, L.nblk, max_policy, hdr);
     prof_mark(KK_SCAN, false, s);
     prof_mark(KK_WRITE_IDX, true, s);
-    k_write_idx<<<L.nblk, kThreads, 0, s>>>(keep, cu, R, N, blkoff, targets, V,
+    k_write_idx<<<L.nblk, kThreads, 0, s>>>(keep, cu, R, N, blkoff, L.nblk, targets, V,
                                              reinterpret_cast<int32_t*>(ws + L.idx),
                                              reinterpret_cast<int32_t*>(ws + L.tokr),
                                              reinterpret_cast<int32_t*>(ws + L.ytgt),
@@ -371,7 +404,7 @@ hipError_t launch_compact(const uint8_t* mask, const int32_t* cu, const int32_t*
   if (R > 0) {
     prof_mark(KK_ROLLOUT_OFFSETS, true, s);
     k_rollout_offsets<<<blocks_for(R, kThreads), kThreads, 0, s>>>(
-        cu, R, N, reinterpret_cast<const int32_t*>(ws + L.idx), hdr,
+        cu, R, N, reinterpret_cast<const int32_t*>(ws + L.idx), zero_adv, hdr,
         reinterpret_cast<int32_t*>(ws + L.rstart), reinterpret_cast<int32_t*>(ws + L.rnpol));
     prof_mark(KK_ROLLOUT_OFFSETS, false, s);
   }

@@ -175,7 +175,7 @@ __global__ void __launch_bounds__(256) k_hidden_t(const uint16_t* hc, int d, con
                                                   const WsHeader* hdr, int64_t c0, int64_t Mc, uint16_t* ht,
                                                   int64_t ldt) {
   __shared__ __attribute__((aligned(16))) uint16_t tile[64][64 + 8];
-  int64_t rc = (int64_t)hdr->n_eff - c0;
+  int64_t rc = (int64_t)hdr->n_grad - c0;  // rows with a surrogate gradient
   rc = rc < 0 ? 0 : (rc > Mc ? Mc : rc);
   const int64_t rpad = (rc + kKAlign - 1) / kKAlign * kKAlign;
   const int64_t t0 = (int64_t)blockIdx.x * 64;
@@ -417,7 +417,7 @@ __device__ __forceinline__ void dz_tile(const DzParams& p, int vt, int64_t t0, i
 template <typename T, bool ENT>
 __global__ void __launch_bounds__(256, 5) k_dz(DzParams p) {
   if (p.ndz && blockIdx.x == 0 && blockIdx.y == 0 && threadIdx.x == 0) atomicAdd(p.ndz, 1);
-  int64_t rc = (int64_t)p.hdr->n_eff - p.c0;
+  int64_t rc = (int64_t)p.hdr->n_grad - p.c0;  // rows with a surrogate gradient
   rc = rc < 0 ? 0 : (rc > p.Mc ? p.Mc : rc);
   const int64_t rpad = (rc + kKAlign - 1) / kKAlign * kKAlign;
   const int64_t t0 = (int64_t)blockIdx.y * 64;
@@ -433,7 +433,7 @@ template <typename T>
 __global__ void __launch_bounds__(256) k_dz_flagged(DzParams p) {
   if (*p.fb == 0) return;
   if (p.ndz && blockIdx.x == 0 && threadIdx.x == 0) atomicAdd(p.ndz, 1);
-  int64_t rc = (int64_t)p.hdr->n_eff - p.c0;
+  int64_t rc = (int64_t)p.hdr->n_grad - p.c0;  // rows with a surrogate gradient
   rc = rc < 0 ? 0 : (rc > p.Mc ? p.Mc : rc);
   const int64_t rpad = (rc + kKAlign - 1) / kKAlign * kKAlign;
   const int nvt = (int)(p.Vp / kVocabTile);
@@ -553,6 +553,7 @@ __global__ void __launch_bounds__(1024) k_loss_final(LossParams p) {
       st.n_policy_tokens = n_eff;
       st.n_chunks = p.nchunks;
       st.n_dz_chunks = p.hdr->n_dz_chunks;
+      st.n_grad_tokens = p.hdr->n_grad;
       *p.stats = st;
     }
   }
@@ -562,10 +563,12 @@ __global__ void __launch_bounds__(1024) k_loss_final(LossParams p) {
 template <typename T>
 __global__ void __launch_bounds__(256)
 k_zero_fill(const uint8_t* keep, int64_t N, int d, T* dh, float* o1, float* o2, float* o3) {
+  // keep 0: not trained (dh row and per-token outputs 0); 2: trained with a zero surrogate gradient
+  // (dh row 0, per-token outputs kept); 1: trained
   const int64_t t = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (t >= N || keep[t]) return;
+  if (t >= N || keep[t] == 1) return;
   const int lane = threadIdx.x & 63;
-  if (lane == 0) {
+  if (lane == 0 && keep[t] == 0) {
     if (o1) o1[t] = 0.0f;
     if (o2) o2[t] = 0.0f;
     if (o3) o3[t] = 0.0f;
@@ -593,7 +596,7 @@ hipError_t launch_transpose_w(int dtype, const void* W, void* WT, int V, int64_t
 
 hipError_t launch_gather(int dtype, const void* hidden, int d, const int32_t* idx, const WsHeader* hdr, int64_t c0,
                          int64_t Mc, void* hc, void* ht, int64_t ldt, bool want_ht, hipStream_t s) {
-  dim3 grid((unsigned)(Mc / 64), (unsigned)((d + 63) / 64));
+  dim3 grid((unsigned)((Mc + 63) / 64), (unsigned)((d + 63) / 64));
   prof_mark(KK_GATHER, true, s);
   if (dtype == RLK_DTYPE_BF16)
     k_gather<uint16_t><<<grid, 256, 0, s>>>((const uint16_t*)hidden, d, idx, hdr, c0, Mc, (uint16_t*)hc,
@@ -632,7 +635,7 @@ hipError_t launch_combine(const TokenParams& p, hipStream_t s) {
 }
 
 hipError_t launch_dz(int dtype, const DzParams& p, hipStream_t s) {
-  const int64_t nvt = p.Vp / kVocabTile, ntb = p.Mc / 64;
+  const int64_t nvt = p.Vp / kVocabTile, ntb = (p.Mc + 63) / 64;
   prof_mark(KK_DZ, true, s);
   if (p.fb) {
     const unsigned grid = (unsigned)std::min<int64_t>(nvt * ntb, kDzBlocks);

@@ -18,8 +18,8 @@ namespace rlk {
 
 // Layouts the Python binding mirrors.
 static_assert(sizeof(rlk_batch_t) == 40, "rlk_batch_t layout");
-static_assert(sizeof(rlk_pg_params_t) == 72, "rlk_pg_params_t layout");
-static_assert(sizeof(rlk_pg_stats_t) == 56, "rlk_pg_stats_t layout");
+static_assert(sizeof(rlk_pg_params_t) == 80, "rlk_pg_params_t layout");
+static_assert(sizeof(rlk_pg_stats_t) == 64, "rlk_pg_stats_t layout");
 
 namespace {
 
@@ -190,7 +190,25 @@ DhTail plan_dh_tail(int64_t rows, int64_t d, int64_t kbytes) {
   return t;
 }
 
-rlk_status_t layout(const rlk_batch_t* b, bool bwd, int64_t chunk_rows, WsLayout& L) {
+// Chunk c of the loop: first compacted row and capacity (rows the chunk's kernels may cover).
+struct ChunkSpan {
+  int64_t c0, rows;
+};
+ChunkSpan chunk_span(const WsLayout& L, int c) {
+  if (c < L.n1) {
+    const int64_t c0 = (int64_t)c * L.Mc1;
+    return {c0, c0 < L.g_rows ? std::min(L.Mc1, L.g_rows - c0) : L.Mc1};
+  }
+  return {L.g_rows + (int64_t)(c - L.n1) * L.Mc2, L.Mc2};
+}
+
+// The caller's count of tokens with a possible surrogate gradient, when the backward skips the others.
+int64_t grad_hint(const rlk_pg_params_t* p) {
+  if (!p || p->grad_tokens <= 0) return 0;
+  return p->entropy_coef == 0.0f && p->kl_coef == 0.0f && !p->token_adv ? p->grad_tokens : 0;
+}
+
+rlk_status_t layout(const rlk_batch_t* b, bool bwd, int64_t chunk_rows, int64_t grad_tokens, WsLayout& L) {
   const int64_t esz = b->dtype == RLK_DTYPE_BF16 ? 2 : 4;
   const int64_t N = b->N, R = b->R, d = b->d, V = b->V;
   L.Vp = roundup(V, kVocabTile);
@@ -213,17 +231,32 @@ rlk_status_t layout(const rlk_batch_t* b, bool bwd, int64_t chunk_rows, WsLayout
   }
   // rows the chunk loop has to cover: all N, or the caller's bound on the trained tokens
   const int64_t B = b->max_policy_tokens > 0 ? std::min<int64_t>(b->max_policy_tokens, N) : N;
-  if (b->max_policy_tokens > 0 && B > 0) Mc = plan_chunk_rows(B, Mc, d, L.Vp);
+  const int64_t cap = Mc;
+  if (b->max_policy_tokens > 0 && B > 0) Mc = plan_chunk_rows(B, cap, d, L.Vp);
   L.Mc = Mc;
   L.rows_bound = B;
   L.nchunks = (int32_t)((B + Mc - 1) / Mc);
   if (bwd && L.nchunks < 1) L.nchunks = 1;
+  L.n1 = L.nchunks;
+  L.Mc1 = L.Mc2 = Mc;
+  L.g_rows = B;
+  if (bwd && b->max_policy_tokens > 0 && grad_tokens > 0 && grad_tokens < B) {
+    // the tokens with a gradient come first in the compacted list: chunks planned over them, then
+    // over the rest (whose backward kernels find no rows and return)
+    const int64_t G = grad_tokens;
+    L.Mc1 = plan_chunk_rows(G, cap, d, L.Vp);
+    L.Mc2 = plan_chunk_rows(B - G, cap, d, L.Vp);
+    L.n1 = (int32_t)((G + L.Mc1 - 1) / L.Mc1);
+    L.g_rows = G;
+    L.nchunks = L.n1 + (int32_t)((B - G + L.Mc2 - 1) / L.Mc2);
+    L.Mc = Mc = std::max(L.Mc1, L.Mc2);
+  }
 
   Alloc a;
   L.hdr = a.take(sizeof(WsHeader));
   L.keep = a.take((size_t)N);
-  L.blkcnt = a.take((size_t)L.nblk * 4);
-  L.blkoff = a.take((size_t)L.nblk * 4);
+  L.blkcnt = a.take((size_t)L.nblk * 8);  // two halves: tokens with and without a surrogate gradient
+  L.blkoff = a.take((size_t)L.nblk * 8);
   L.idx = a.take((size_t)N * 4);
   L.tokr = a.take((size_t)N * 4);
   L.ytgt = a.take((size_t)N * 4);
@@ -265,8 +298,10 @@ rlk_status_t layout(const rlk_batch_t* b, bool bwd, int64_t chunk_rows, WsLayout
     size_t pb = std::max({splitk_bytes(Mc, d, L.sk_dh), splitk_bytes(V, d, L.sk_dw),
                           splitk_bytes(V - L.dw_m0, d, L.sk_dwt)});
     if (L.sk_dh.s == 1 && b->max_policy_tokens > 0)
-      for (int64_t c0 = 0; c0 < B; c0 += Mc) {
-        const DhTail t = plan_dh_tail(std::min(Mc, B - c0), d, L.Vp * esz);
+      for (int c = 0; c < L.nchunks; ++c) {
+        const ChunkSpan cs = chunk_span(L, c);
+        if (cs.c0 >= B) break;
+        const DhTail t = plan_dh_tail(std::min(cs.rows, B - cs.c0), d, L.Vp * esz);
         if (t.m0 > 0) pb = std::max(pb, splitk_bytes(t.rows, d, t.sk));
       }
     if (pb > 0) L.part = a.take(pb);
@@ -462,7 +497,7 @@ rlk_status_t rlk_workspace_size(const rlk_batch_t* b, const rlk_pg_params_t* p, 
   rlk_status_t st = check_batch(b);
   if (st) return st;
   WsLayout L;
-  st = layout(b, p != nullptr, p ? p->chunk_rows : 0, L);
+  st = layout(b, p != nullptr, p ? p->chunk_rows : 0, grad_hint(p), L);
   if (st) return st;
   *bytes = L.total;
   return RLK_OK;
@@ -484,7 +519,7 @@ rlk_status_t rlk_logprob_fwd(const rlk_batch_t* b, const void* hidden, const voi
   if (!W) return fail(RLK_EINVAL, "W is NULL");
   if (misaligned16(hidden) || misaligned16(W)) return fail(RLK_EINVAL, "hidden and W must be 16-byte aligned");
   WsLayout L;
-  st = layout(b, false, 0, L);
+  st = layout(b, false, 0, 0, L);
   if (st) return st;
   st = check_ws(ws, ws_bytes, L.total);
   if (st) return st;
@@ -495,7 +530,8 @@ rlk_status_t rlk_logprob_fwd(const rlk_batch_t* b, const void* hidden, const voi
 
   RLK_TRY(launch_begin(reinterpret_cast<int32_t*>(hdr), b->cu_seqlens, b->R, N, s), "begin");
   if (N == 0) return finish(hipSuccess, "", ws, s);
-  RLK_TRY(launch_compact(mask, b->cu_seqlens, nullptr, b->R, N, targets, b->V, b->max_policy_tokens, w, L, s),
+  RLK_TRY(launch_compact(mask, b->cu_seqlens, nullptr, b->R, N, targets, b->V, b->max_policy_tokens, nullptr, w, L,
+                         s),
           "compact");
   for (int c = 0; c < L.nchunks; ++c) {
     const int64_t c0 = (int64_t)c * L.Mc;
@@ -559,7 +595,7 @@ rlk_status_t rlk_compact(const rlk_batch_t* b, const uint8_t* mask, const int32_
   if (!n_eff || (b->N > 0 && (!idx || !tok_rollout)) || (b->R > 0 && !n_pol))
     return fail(RLK_EINVAL, "idx, tok_rollout, n_pol or n_eff is NULL");
   WsLayout L;
-  st = layout(b, false, 0, L);
+  st = layout(b, false, 0, 0, L);
   if (st) return st;
   st = check_ws(ws, ws_bytes, L.total);
   if (st) return st;
@@ -567,7 +603,8 @@ rlk_status_t rlk_compact(const rlk_batch_t* b, const uint8_t* mask, const int32_
   char* w = static_cast<char*>(ws);
   WsHeader* hdr = reinterpret_cast<WsHeader*>(w + L.hdr);
   RLK_TRY(launch_begin(reinterpret_cast<int32_t*>(hdr), b->cu_seqlens, b->R, b->N, s), "begin");
-  RLK_TRY(launch_compact(mask, b->cu_seqlens, group_ids, b->R, b->N, targets, b->V, b->max_policy_tokens, w, L, s),
+  RLK_TRY(launch_compact(mask, b->cu_seqlens, group_ids, b->R, b->N, targets, b->V, b->max_policy_tokens, nullptr,
+                         w, L, s),
           "compact");
   if (b->N > 0) {
     RLK_TRY(hipMemcpyAsync(idx, w + L.idx, (size_t)b->N * 4, hipMemcpyDeviceToDevice, s), "copy idx");
@@ -630,7 +667,8 @@ rlk_status_t rlk_pg_loss_fwd_bwd(const rlk_batch_t* b, const void* hidden, const
   if (!(p->kl_coef >= 0.0f) || !isfinite(p->kl_coef)) return fail(RLK_EINVAL, "kl_coef must be finite and >= 0");
   if (p->kl_coef > 0.0f && !p->ref_logp) return fail(RLK_EINVAL, "kl_coef > 0 needs ref_logp");
   WsLayout L;
-  st = layout(b, true, p->chunk_rows, L);
+  if (p->grad_tokens < 0) return fail(RLK_EINVAL, "grad_tokens must be >= 0");
+  st = layout(b, true, p->chunk_rows, grad_hint(p), L);
   if (st) return st;
   st = check_ws(ws, ws_bytes, L.total);
   if (st) return st;
@@ -644,12 +682,17 @@ rlk_status_t rlk_pg_loss_fwd_bwd(const rlk_batch_t* b, const void* hidden, const
   auto I = [&](size_t off) { return reinterpret_cast<int32_t*>(w + off); };
 
   RLK_TRY(launch_begin(reinterpret_cast<int32_t*>(hdr), b->cu_seqlens, R, N, s), "begin");
-  RLK_TRY(launch_compact(mask, b->cu_seqlens, group_ids, R, N, targets, b->V, b->max_policy_tokens, w, L, s),
-          "compact");
   RLK_TRY(launch_advantage(R, rewards, group_ids, p->adv_eps, I(L.members), I(L.gstart), I(L.gidx), I(L.gsize),
                            reinterpret_cast<double*>(w + L.gmu), reinterpret_cast<double*>(w + L.gsig), I(L.geq),
                            F(L.adv), hdr, s),
           "advantage");
+  // With the advantage-weighted surrogate as the only term (no entropy bonus, KL term or per-token
+  // advantages), a rollout of advantage exactly 0 has an exactly zero gradient: its tokens go last in
+  // the compacted list and the backward covers the tokens before them.
+  const bool zero_grad_skip = p->entropy_coef == 0.0f && p->kl_coef == 0.0f && !p->token_adv;
+  RLK_TRY(launch_compact(mask, b->cu_seqlens, group_ids, R, N, targets, b->V, b->max_policy_tokens,
+                         zero_grad_skip ? F(L.adv) : nullptr, w, L, s),
+          "compact");
   RLK_TRY(launch_transpose_w(b->dtype, W, w + L.wt, b->V, L.Vp, b->d, L.ldw, s), "transpose_w");
   // Token-reference layout (bf16 without an entropy term): the forward stores q against each token's
   // target logit and writes q^T as well; the combine makes dz = diag(s) q exact, the dhidden GEMM and
@@ -659,12 +702,13 @@ rlk_status_t rlk_pg_loss_fwd_bwd(const rlk_batch_t* b, const void* hidden, const
   const size_t esz = b->dtype == RLK_DTYPE_BF16 ? 2 : 4;
   int32_t* fb = &hdr->ref_fallback;
   for (int c = 0; c < L.nchunks; ++c) {
-    const int64_t c0 = (int64_t)c * L.Mc;
-    RLK_TRY(launch_gather(b->dtype, hidden, b->d, I(L.idx), hdr, c0, L.Mc, w + L.hc, w + L.ht, L.ldt, !ref_layout,
+    const ChunkSpan cs = chunk_span(L, c);
+    const int64_t c0 = cs.c0, Mcc = cs.rows;
+    RLK_TRY(launch_gather(b->dtype, hidden, b->d, I(L.idx), hdr, c0, Mcc, w + L.hc, w + L.ht, L.ldt, !ref_layout,
                           s),
             "gather");
     if (ref_layout)
-      RLK_TRY(launch_target_logit(w + L.hc, b->d, W, I(L.ytgt), hdr, c0, L.Mc, b->V, inv_temperature(b), F(L.zr),
+      RLK_TRY(launch_target_logit(w + L.hc, b->d, W, I(L.ytgt), hdr, c0, Mcc, b->V, inv_temperature(b), F(L.zr),
                                   fb, s),
               "target_logit");
     GemmArgs g = {};
@@ -673,11 +717,11 @@ rlk_status_t rlk_pg_loss_fwd_bwd(const rlk_batch_t* b, const void* hidden, const
     g.lda = b->d;
     g.ldb = b->d;
     g.M = b->V;
-    g.N = (int)L.Mc;
+    g.N = (int)Mcc;
     g.K = b->d;
     g.hdr = hdr;
     g.c0 = c0;
-    g.Mc = L.Mc;
+    g.Mc = Mcc;
     g.ytgt = I(L.ytgt);
     g.zy = F(L.zy);
     g.pm = F(L.pm);
@@ -699,7 +743,7 @@ rlk_status_t rlk_pg_loss_fwd_bwd(const rlk_batch_t* b, const void* hidden, const
     tp.inv_tau = inv_temperature(b);
     tp.hdr = hdr;
     tp.c0 = c0;
-    tp.Mc = L.Mc;
+    tp.Mc = Mcc;
     tp.nvt = L.nvt;
     tp.pm = g.pm;
     tp.ps = g.ps;
@@ -746,7 +790,7 @@ rlk_status_t rlk_pg_loss_fwd_bwd(const rlk_batch_t* b, const void* hidden, const
     DzParams dp = {};
     dp.hdr = hdr;
     dp.c0 = c0;
-    dp.Mc = L.Mc;
+    dp.Mc = Mcc;
     dp.Vp = L.Vp;
     dp.ldq = L.ldq;
     dp.ldt = L.ldt;
@@ -765,19 +809,19 @@ rlk_status_t rlk_pg_loss_fwd_bwd(const rlk_batch_t* b, const void* hidden, const
     dp.ndz = &hdr->n_dz_chunks;
     RLK_TRY(launch_dz(b->dtype, dp, s), "dz");
     if (ref_layout)
-      RLK_TRY(launch_hidden_t(w + L.hc, b->d, F(L.st), fb, hdr, c0, L.Mc, w + L.ht, L.ldt, s), "hidden_t");
+      RLK_TRY(launch_hidden_t(w + L.hc, b->d, F(L.st), fb, hdr, c0, Mcc, w + L.ht, L.ldt, s), "hidden_t");
 
     GemmArgs h = {};
     h.A = w + L.q;
     h.B = w + L.wt;
     h.lda = L.ldq;
     h.ldb = L.ldw;
-    h.M = (int)L.Mc;
+    h.M = (int)Mcc;
     h.N = b->d;
     h.K = (int)L.Vp;
     h.hdr = hdr;
     h.c0 = c0;
-    h.Mc = L.Mc;
+    h.Mc = Mcc;
     h.out = dhidden;
     h.idx = I(L.idx);
     h.ldo = b->d;
@@ -787,7 +831,7 @@ rlk_status_t rlk_pg_loss_fwd_bwd(const rlk_batch_t* b, const void* hidden, const
     }
     set_split(h, L.sk_dh, w + L.part);
     const DhTail dt = L.sk_dh.s == 1 && b->max_policy_tokens > 0
-                          ? plan_dh_tail(std::min(L.Mc, L.rows_bound - c0), b->d, L.Vp * esz)
+                          ? plan_dh_tail(std::min(Mcc, L.rows_bound - c0), b->d, L.Vp * esz)
                           : DhTail{};
     if (dt.m0 > 0) {
       // the tile rows of the partial last wave, split over K: the same GEMM on the chunk rows from
@@ -796,7 +840,7 @@ rlk_status_t rlk_pg_loss_fwd_bwd(const rlk_batch_t* b, const void* hidden, const
       t.A = w + L.q + (size_t)dt.m0 * L.ldq * esz;
       t.M = (int)dt.rows;
       t.c0 = c0 + dt.m0;
-      t.Mc = dt.rows;
+      t.Mc = std::min(dt.rows, Mcc - dt.m0);  // a ragged chunk ends inside the last tile row
       if (t.rs) t.rs += dt.m0;
       set_split(t, dt.sk, w + L.part);
       h.M = (int)dt.m0;
@@ -814,10 +858,10 @@ rlk_status_t rlk_pg_loss_fwd_bwd(const rlk_batch_t* b, const void* hidden, const
     k.ldb = L.ldt;
     k.M = b->V;
     k.N = b->d;
-    k.K = (int)L.Mc;
+    k.K = (int)Mcc;
     k.hdr = hdr;
     k.c0 = c0;
-    k.Mc = L.Mc;
+    k.Mc = Mcc;
     k.dw = dW;
     k.ldo = b->d;
     k.accumulate = p->accumulate_dW;

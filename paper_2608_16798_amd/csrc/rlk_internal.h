@@ -101,9 +101,10 @@ struct WsHeader {
   int32_t n_eff;     // number of trained tokens
   int32_t n_groups;  // Q
   int32_t n_valid;   // non-excluded rollouts
+  int32_t n_grad;    // leading trained tokens of the compacted list that carry a surrogate gradient
   int32_t ref_fallback;  // current chunk: 1 = its token-reference layout does not hold, dz explicit
   int32_t n_dz_chunks;   // chunks whose dz was formed explicitly
-  int32_t pad[58];
+  int32_t pad[57];
 };
 
 // Byte offsets of the workspace segments (all 256-aligned).
@@ -132,6 +133,10 @@ struct WsLayout {
   int64_t dw_m0 = 0;
   SplitK sk_dwt = {1, 1};
   int64_t rows_bound = 0;          // trained tokens the chunk loop covers (N, or the caller's bound)
+  // chunk c < n1 covers [c Mc1, min((c + 1) Mc1, g_rows)); the others [g_rows + (c - n1) Mc2, + Mc2)
+  // (without a hint: n1 = nchunks, Mc1 = Mc2 = Mc, g_rows = rows_bound)
+  int64_t Mc1 = 0, Mc2 = 0, g_rows = 0;
+  int32_t n1 = 0;
   int64_t Mc = 0;                  // chunk rows
   int64_t Vp = 0;                  // vocabulary padded to 256
   // Row strides (elements) of the chunk buffers read by the gradient GEMMs: padded by 64 when the
@@ -144,9 +149,11 @@ struct WsLayout {
 
 // ---- launchers (k_segment.hip) ----
 hipError_t launch_begin(int32_t* status_hdr, const int32_t* cu, int R, int64_t N, hipStream_t s);
+// zero_adv [R] (may be NULL): the rollouts' advantages; the tokens of a rollout whose advantage is
+// exactly 0 are listed after all others (n_grad = the count before them; NULL: n_grad = n_eff).
 hipError_t launch_compact(const uint8_t* mask, const int32_t* cu, const int32_t* gid, int R, int64_t N,
-                          const int32_t* targets, int V, int32_t max_policy, char* ws, const WsLayout& L,
-                          hipStream_t s);
+                          const int32_t* targets, int V, int32_t max_policy, const float* zero_adv, char* ws,
+                          const WsLayout& L, hipStream_t s);
 // members [R] (rollouts of the kept groups, group by group), gstart [R + 1] (run starts), gidx [R],
 // and per group gsize, gmu, gsig, geq [R]; R <= kMaxRollouts.
 hipError_t launch_advantage(int R, const float* rewards, const int32_t* gid, float adv_eps, int32_t* members,

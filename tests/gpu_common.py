@@ -104,7 +104,7 @@ def run_gpu(inst, params, *, gid=None, mask="default", dW=None, ws=None, aux=Non
     torch.cuda.synchronize()
     flags = rlk.check_status(ws)
     return dict(loss=float(loss.item()), dh=dh, dW=dWo, logp=logp, ent=ent, stats=rlk.stats_from_tensor(stats),
-                flags=flags, ws=ws)
+                flags=flags, ws=ws, token_adv=token_adv is not None)
 
 
 def run_oracle(inst, params, *, grads=True, aux=None, token_adv=None, temperature=1.0):
@@ -194,7 +194,16 @@ def compare_full(inst, gpu, ref, params, tag=""):
     assert st["n_chunks"] >= 1 and 0 <= st["n_dz_chunks"] <= st["n_chunks"]
     if not ref_layout(cfg, params):
         assert st["n_dz_chunks"] == st["n_chunks"]
+    # the backward covers the tokens with a surrogate gradient: without an entropy term, a KL term or
+    # per-token advantages, those of rollouts with a non-zero advantage
+    assert st["n_grad_tokens"] == expected_grad_tokens(ref, params, gpu.get("token_adv", False))
     return m
+
+
+def expected_grad_tokens(ref, params, token_adv):
+    if params.entropy_coef == 0.0 and params.kl_coef == 0.0 and not token_adv:
+        return int(np.count_nonzero(ref["adv_tok"]))
+    return int(ref["idx"].shape[0])
 
 
 def ref_layout(cfg, params):

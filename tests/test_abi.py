@@ -37,7 +37,7 @@ def test_exports_every_declared_symbol(lib):
 
 
 def test_version_and_strings(lib):
-    assert lib.rlk_version() == 6
+    assert lib.rlk_version() == 7
     assert lib.rlk_status_string(rlk.RLK_EWORKSPACE).decode().startswith("workspace")
     assert lib.rlk_kernel_kind_name(10).decode() == "fwd_lse_gemm"
 
@@ -120,7 +120,7 @@ def test_host_validation(lib):
         p.rollout_logp = ro
         p.ref_logp = rf
         assert lib.rlk_pg_loss_fwd_bwd(*args(p)) == rlk.RLK_EINVAL, (kw, ro, rf)
-    assert ctypes.sizeof(rlk.PgParams) == 72 and ctypes.sizeof(rlk.PgStats) == 56
+    assert ctypes.sizeof(rlk.PgParams) == 80 and ctypes.sizeof(rlk.PgStats) == 64
     assert ctypes.sizeof(rlk.Batch) == 40
     for tau in (-1.0, float("inf"), float("nan")):
         bad = _batch(cfg)

@@ -105,3 +105,29 @@ def test_advantage_ppo_and_value_head_reject():
         rlk.value_head_bwd(h, torch.zeros(d, dtype=torch.bfloat16), m, cu, None, torch.zeros(N + 3))
     with pytest.raises(ValueError, match="must be a GPU tensor"):
         rlk.value_head_fwd(h, torch.zeros(d, dtype=torch.bfloat16), 0.0, m, cu)
+
+
+# The chunk-planning hint counts the trained tokens in groups of unequal rewards; the oracle's group
+# advantage (Sec. 2.3.1) is exactly 0 for the rollouts of the other groups and, with continuous rewards,
+# nonzero for every rollout of a mixed group, so the two counts agree.
+@pytest.mark.parametrize("seed", [0, 1, 2])
+def test_grad_token_hint_counts_the_oracle_nonzero_advantage_tokens(seed):
+    import numpy as np
+
+    import oracle as O
+
+    rng = np.random.default_rng(seed)
+    R = 24
+    lens = rng.integers(1, 40, R)
+    cu = np.concatenate([[0], np.cumsum(lens)]).astype(np.int64)
+    mask = (rng.random(cu[-1]) < 0.7).astype(np.uint8)
+    gid = rng.integers(-1, 6, R).astype(np.int32)          # -1: excluded rollouts
+    rewards = rng.standard_normal(R)
+    for g in (1, 3):
+        rewards[gid == g] = 0.5 * g                        # two all-equal groups
+    adv = O.group_advantage(rewards, gid)["adv"]
+    tok_adv = np.repeat(adv, lens)
+    tok_live = np.repeat(gid >= 0, lens)
+    expect = int(((mask == 1) & tok_live & (tok_adv != 0.0)).sum())
+    assert rlk.grad_token_hint(mask, cu, rewards, gid) == expect
+    assert rlk.grad_token_hint(mask, cu, np.zeros(R), gid) == 0

@@ -10,7 +10,7 @@ import numpy as np
 import pytest
 
 from gpu_common import (TOL_GRAD, TOL_LOSS, aux_logps, loss_error, TOL_LOGP, O, WL, build_instance, compare_full, ensure_library, log,
-                        params_for, ref_layout, rel_fro, rlk, run_gpu, run_oracle, to_host, with_far_target)
+                        expected_grad_tokens, params_for, ref_layout, rel_fro, rlk, run_gpu, run_oracle, to_host, with_far_target)
 
 pytestmark = pytest.mark.gpu
 
@@ -566,3 +566,82 @@ def test_dhidden_tail_split_over_k():
         log(f"dhidden tail split: N_eff={n_eff} bound={bound}")
         gpu = run_gpu(inst, p, max_policy_tokens=bound)
         compare_full(inst, gpu, ref, p, tag=f"dh tail bound={bound}")
+
+
+# Zero-advantage rollouts (Sec. 2.3.2: every rollout of an all-equal group has advantage 0): with the
+# surrogate as the only term their tokens get the forward but skip the backward GEMMs; log-probs and
+# entropies are still written for them, their dhidden rows are exactly 0, and a batch where no token
+# carries a gradient overwrites dW with zeros (or leaves an accumulated dW as it was).
+def test_zero_advantage_rollouts_skip_the_backward():
+    import torch
+
+    cfg = WL.scaled_config("qwen8b_bf16")
+    inst = build_instance(cfg)
+    st = inst["st"]
+    gid = st.group_ids
+    g0 = gid[gid >= 0][0]
+    rewards = st.rewards.copy()
+    rewards[gid == g0] = 1.0                       # one all-equal group
+    inst1 = dict(inst, rewards=torch.as_tensor(rewards, device="cuda"),
+                 st=__import__("dataclasses").replace(st, rewards=rewards))
+    p = params_for(cfg, chunk_rows=256)
+    gpu = run_gpu(inst1, p)
+    ref = run_oracle(inst1, p)
+    compare_full(inst1, gpu, ref, p, tag="zero-advantage group")
+    zero_rows = ref["idx"][ref["adv_tok"] == 0]
+    assert zero_rows.size > 0 and gpu["stats"]["n_grad_tokens"] == ref["idx"].size - zero_rows.size
+    rows_t = torch.as_tensor(zero_rows, device="cuda")
+    assert float(gpu["dh"][rows_t].float().abs().max()) == 0.0
+    assert float(gpu["logp"][rows_t].abs().min()) > 0.0
+    # the same batch with an entropy term: no skipping
+    pe = params_for(cfg, chunk_rows=256, entropy_coef=0.01)
+    ge = run_gpu(inst1, pe)
+    assert ge["stats"]["n_grad_tokens"] == ref["idx"].size
+
+    # every group all-equal: nothing carries a gradient
+    rewards_all = np.full_like(st.rewards, 0.25)
+    inst2 = dict(inst, rewards=torch.as_tensor(rewards_all, device="cuda"),
+                 st=__import__("dataclasses").replace(st, rewards=rewards_all))
+    g2 = run_gpu(inst2, p)
+    ref2 = run_oracle(inst2, p)
+    compare_full(inst2, g2, ref2, p, tag="all groups equal")
+    assert g2["stats"]["n_grad_tokens"] == 0 and g2["loss"] == 0.0
+    assert float(g2["dW"].abs().max()) == 0.0 and float(g2["dh"].float().abs().max()) == 0.0
+    dW0 = torch.randn(inst["W"].shape, device="cuda", dtype=torch.float32)
+    g3 = run_gpu(inst2, params_for(cfg, chunk_rows=256, accumulate_dW=True), dW=dW0.clone())
+    assert torch.equal(g3["dW"], dW0)
+
+
+# The host hint of gradient-carrying tokens (groups of unequal rewards) only plans the chunk loop:
+# chunks over the first grad_tokens compacted rows, then over the rest.  Exact, too small, too large
+# and out-of-range hints, and a hint the loss cannot use (an entropy term), all give the oracle's
+# results; the exact hint puts the boundary at N_grad.
+def test_grad_token_hint_only_plans_the_chunks():
+    import torch
+
+    base = WL.scaled_config("small_bf16")
+    cfg = base.with_(name="small_bf16_d1024_V4096", groups=4, rollouts_per_group=8, len_min=512, len_max=1024,
+                     d=1024, V=4096, w_std=1.0 / 32.0)
+    inst = build_instance(cfg)
+    st = inst["st"]
+    gid = st.group_ids
+    rewards = st.rewards.copy()
+    live = np.unique(gid[gid >= 0])
+    for g in live[1::2]:
+        rewards[gid == g] = 1.0                    # every other group all-equal
+    st1 = __import__("dataclasses").replace(st, rewards=rewards)
+    inst1 = dict(inst, rewards=torch.as_tensor(rewards, device="cuda"), st=st1)
+    n_eff = int(O.compact(st.mask, st.cu_seqlens, st.group_ids)[0].shape[0])
+    G = rlk.grad_token_hint(st.mask, st.cu_seqlens, rewards, gid)
+    assert 0 < G < n_eff
+    p0 = params_for(cfg, chunk_rows=4096)
+    ref = run_oracle(inst1, p0)
+    assert G == expected_grad_tokens(ref, p0, False)
+    for hint in (G, G // 3, min(G + 3000, n_eff - 1), 1, n_eff - 1, n_eff, 10 * n_eff):
+        p = params_for(cfg, chunk_rows=4096, grad_tokens=hint)
+        log(f"grad-token hint {hint} (N_grad={G}, N_eff={n_eff})")
+        gpu = run_gpu(inst1, p, max_policy_tokens=n_eff)
+        compare_full(inst1, gpu, ref, p, tag=f"grad hint {hint}")
+    pe = params_for(cfg, chunk_rows=4096, entropy_coef=0.01, grad_tokens=G)
+    gpu = run_gpu(inst1, pe, max_policy_tokens=n_eff)
+    compare_full(inst1, gpu, run_oracle(inst1, pe), pe, tag="grad hint with an entropy term")
