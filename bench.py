@@ -290,25 +290,31 @@ def hbm_kernel_summary(fetch_csv, write_csv, workload, copy_mib, cmd_fetch, cmd_
 
     import workloads as WL
 
+    import paper_2608_16798_amd as rlk
+
     cfg = WL.get_config(workload)
     st = WL.make_structure(cfg)
-    n_eff = int(np.asarray(st.mask, dtype=np.int64).sum())
+    n_eff = host_policy_tokens(st)
+    # rows past the backward: those of zero-advantage rollouts when the surrogate is the only term
+    n_grad = rlk.grad_token_hint(st.mask, st.cu_seqlens, st.rewards, st.group_ids) if cfg.entropy_coef == 0.0 else n_eff
     esz = 2 if cfg.dtype == "bf16" else 4
     vp = (cfg.V + 255) // 256 * 256
     # token-reference layout (bf16 without an entropy term): no explicit dz pass unless a chunk is
     # flagged, the gather writes h_c only, and the s-scaled h_c^T comes after the combine
     ref = cfg.dtype == "bf16" and cfg.entropy_coef == 0.0
     hrow = n_eff * cfg.d * esz
-    alg = {"k_dz": 3 * n_eff * vp * esz, "k_dz_flagged": 0, "k_gather": (2 if ref else 3) * hrow,
-           "k_target_logit": 2 * hrow, "k_hidden_t": 2 * hrow,
-           "k_transpose_w": (cfg.V + vp) * cfg.d * esz, "k_zero_fill": (st.N - n_eff) * (cfg.d * esz + 8),
+    alg = {"k_dz": 3 * n_grad * vp * esz, "k_dz_flagged": 0, "k_gather": (2 if ref else 3) * hrow,
+           "k_target_logit": 2 * hrow, "k_hidden_t": 2 * n_grad * cfg.d * esz,
+           "k_transpose_w": (cfg.V + vp) * cfg.d * esz,
+           "k_zero_fill": (st.N - n_eff) * (cfg.d * esz + 8) + (n_eff - n_grad) * cfg.d * esz,
            "k_combine": n_eff * (12 * (vp // 256) + 40)}
-    what = {"k_dz": "read q, write dz and dz^T",
+    what = {"k_dz": "read q, write dz and dz^T (N_grad rows)",
             "k_dz_flagged": "dz of flagged chunks only; none expected here, every block exits at once",
             "k_gather": "read h rows, write h_c" + ("" if ref else " and h_c^T"),
             "k_target_logit": "read h_c rows and the target rows of W",
-            "k_hidden_t": "read h_c, write the row-scaled h_c^T",
-            "k_transpose_w": "read W, write W^T", "k_zero_fill": "zero untrained rows of dh, logp, entropy",
+            "k_hidden_t": "read h_c, write the row-scaled h_c^T (N_grad rows)",
+            "k_transpose_w": "read W, write W^T",
+            "k_zero_fill": "zero untrained rows of dh, logp, entropy, and the dh rows past N_grad",
             "k_combine": "read the online-LSE partials, write per-token values"}
 
     def per_kernel(path):
@@ -327,7 +333,7 @@ def hbm_kernel_summary(fetch_csv, write_csv, workload, copy_mib, cmd_fetch, cmd_
     path = os.path.join(PROFILES, f"hbm_kernels_{workload}_traffic.txt")
     with open(path, "w") as f:
         f.write(f"# HBM traffic of the bandwidth-bound kernels on the {workload} workload, one step, rocprofv3 "
-                f"counters (N_eff = {n_eff})\n")
+                f"counters (N_eff = {n_eff}, N_grad = {n_grad})\n")
         f.write(f"# fetch pass: {cmd_fetch}\n# write pass: {cmd_write}\n")
         f.write(f"# summary: python bench.py --traffic-summary <fetch csv> <write csv> --workload {workload} "
                 f"--calibrate-copy-mib {copy_mib}\n")
