@@ -375,7 +375,9 @@ def stats_summary(stats_csv, title, cmd):
 
 def next_rows(cfg, inp, params, steps):
     """Timings of the adjacent paths at the workload's shape: the loss call with truncated
-    importance sampling and the KL term switched on (overhead over the plain call); the PPO path's
+    importance sampling, and with the KL term as well (overheads over the plain call; a KL term
+    gives zero-advantage rollouts a gradient, so that call runs the backward on all N_eff tokens);
+    the PPO path's
     GAE, value loss and linear value head (time and achieved bandwidth on their algorithmic
     bytes); the host prefix-tree packer on a synthetic call log."""
     import numpy as np
@@ -385,16 +387,19 @@ def next_rows(cfg, inp, params, steps):
 
     st = inp["st"]
     N, R, d = st.N, st.R, cfg.d
-    n_eff = int(np.asarray(st.mask, dtype=np.int64).sum())
+    n_eff = host_policy_tokens(st)
     esz = 2 if cfg.dtype == "bf16" else 4
     dev = "cuda"
     g = torch.Generator(device=dev).manual_seed(cfg.seed + 4242)
     loss = torch.empty(1, dtype=torch.float32, device=dev)
     dh = torch.empty_like(inp["h"])
     dW = torch.empty(inp["W"].shape, dtype=torch.float32, device=dev)
-    batch = rlk.make_batch(inp["h"], inp["W"], inp["cu"])
-    pk = rlk.make_params(eps_low=params.eps_low, eps_high=params.eps_high, tis_cap=2.0, kl_coef=0.05)
-    ws = rlk.alloc_workspace(max(rlk.workspace_size(batch, params), rlk.workspace_size(batch, pk)), dev)
+    batch = rlk.make_batch(inp["h"], inp["W"], inp["cu"], max_policy_tokens=n_eff)
+    pt = rlk.make_params(eps_low=params.eps_low, eps_high=params.eps_high, entropy_coef=params.entropy_coef,
+                         tis_cap=2.0, grad_tokens=params.grad_tokens)
+    pk = rlk.make_params(eps_low=params.eps_low, eps_high=params.eps_high, entropy_coef=params.entropy_coef,
+                         tis_cap=2.0, kl_coef=0.05)
+    ws = rlk.alloc_workspace(max(rlk.workspace_size(batch, p) for p in (params, pt, pk)), dev)
     rollout = inp["old"] + 0.1 * torch.randn(N, generator=g, device=dev)
     ref = inp["old"] + 0.2 * torch.randn(N, generator=g, device=dev)
 
@@ -411,12 +416,15 @@ def next_rows(cfg, inp, params, steps):
 
     def loss_call(p, **kw):
         return lambda: rlk.pg_loss_fwd_bwd(inp["h"], inp["W"], inp["targets"], inp["mask"], inp["cu"], inp["old"],
-                                           inp["rewards"], inp["gid"], p, loss=loss, dhidden=dh, dW=dW, ws=ws, **kw)
+                                           inp["rewards"], inp["gid"], p, loss=loss, dhidden=dh, dW=dW, ws=ws,
+                                           max_policy_tokens=n_eff, **kw)
 
-    out = {"workload": cfg.name, "N": N, "N_eff": n_eff}
+    out = {"workload": cfg.name, "N": N, "N_eff": n_eff, "grad_tokens": params.grad_tokens}
     base = timed(loss_call(params), steps)
+    tt = timed(loss_call(pt, rollout_logp=rollout), steps)
     tk = timed(loss_call(pk, rollout_logp=rollout, ref_logp=ref), steps)
     out["loss_call_ms"] = round(base, 3)
+    out["loss_call_tis_ms"] = round(tt, 3)
     out["loss_call_tis_kl_ms"] = round(tk, 3)
     # PPO path
     values = torch.randn(N, generator=g, device=dev)
