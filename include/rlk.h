@@ -132,8 +132,10 @@ typedef struct {
   /* Optional host-known count of the trained tokens whose rollout advantage is not 0 (the tokens
    * that go through the backward when the loss has no entropy term, KL term or per-token
    * advantages; see rlk_pg_loss_fwd_bwd), with max_policy_tokens > 0: the chunk loop then puts a
-   * chunk boundary at that count, so the backward runs on well-filled chunks.  0 = unknown.  It only
-   * plans the chunks: any value gives the same results.  Must be >= 0. */
+   * chunk boundary at that count rounded up to a multiple of 256, so the backward runs on
+   * well-filled chunks.  0 = unknown.  It only plans the chunks: any value gives the same results,
+   * and the workspace size depends on it (query rlk_workspace_size with the same params).
+   * Must be >= 0. */
   int64_t grad_tokens;
 } rlk_pg_params_t;
 
