@@ -645,3 +645,27 @@ def test_grad_token_hint_only_plans_the_chunks():
     pe = params_for(cfg, chunk_rows=4096, entropy_coef=0.01, grad_tokens=G)
     gpu = run_gpu(inst1, pe, max_policy_tokens=n_eff)
     compare_full(inst1, gpu, run_oracle(inst1, pe), pe, tag="grad hint with an entropy term")
+
+
+# Truncated importance sampling scales the surrogate by a constant weight, so a zero-advantage rollout
+# still has an exactly zero gradient and skips the backward; in both aggregation modes the loss
+# normalisers still count its tokens.
+@pytest.mark.parametrize("agg", [rlk.AGG_SEQ, rlk.AGG_TOKEN])
+def test_tis_alone_keeps_the_zero_advantage_skip(agg):
+    import torch
+
+    cfg = WL.scaled_config("qwen8b_bf16")
+    inst = build_instance(cfg)
+    st = inst["st"]
+    gid = st.group_ids
+    rewards = st.rewards.copy()
+    rewards[gid == gid[gid >= 0][-1]] = 0.0        # one all-equal group
+    inst1 = dict(inst, rewards=torch.as_tensor(rewards, device="cuda"),
+                 st=__import__("dataclasses").replace(st, rewards=rewards))
+    aux = aux_logps(inst1)
+    p = params_for(cfg, agg=agg, tis_cap=1.1, chunk_rows=256)
+    gpu = run_gpu(inst1, p, aux=aux)
+    ref = run_oracle(inst1, p, aux=aux)
+    assert 0 < np.mean(ref["tis"] == np.float64(p.tis_cap)) < 1
+    assert np.count_nonzero(ref["adv_tok"] == 0) > 0
+    compare_full(inst1, gpu, ref, p, tag=f"tis, zero-advantage group, agg {agg}")
