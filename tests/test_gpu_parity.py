@@ -348,9 +348,12 @@ def test_full_size_sampled_rows(name, far):
         st = inst["st"]
         log(f"  far target at policy token {far_pos} (row {int(idx[far_pos])}), log-prob {lp_far:.1f}")
     # the benchmark passes the host-known count of trained tokens as the bound (without far: chunks sized
-    # by it, and dhidden tile rows of a partial last wave split over K; with far: chunks over all N)
+    # by it, and dhidden tile rows of a partial last wave split over K; with far: chunks over all N) and
+    # the host count of tokens in groups of unequal rewards as the chunk-planning hint
     bound = 0 if far else int(idx.shape[0])
-    log(f"full-size {name} N={st.N} max_policy_tokens={bound}")
+    if bound:
+        p = params_for(cfg, grad_tokens=rlk.grad_token_hint(st.mask, st.cu_seqlens, st.rewards, st.group_ids))
+    log(f"full-size {name} N={st.N} max_policy_tokens={bound} grad_tokens={p.grad_tokens}")
     gpu = run_gpu(inst, p, max_policy_tokens=bound)
     assert gpu["flags"] == 0
     sg = gpu["stats"]
@@ -364,6 +367,9 @@ def test_full_size_sampled_rows(name, far):
     assert gpu["stats"]["n_policy_tokens"] == idx.shape[0] and gpu["stats"]["n_groups"] == ga["n_groups"]
     omega = O.token_weights(tr, npol, ga["group_index"], ga["G"], ga["n_groups"], p.agg)
     adv_tok = ga["adv"][tr]
+    # surrogate-only loss: the tokens of zero-advantage rollouts skip the backward
+    n_grad = int(np.count_nonzero(adv_tok)) if p.entropy_coef == 0.0 else int(idx.shape[0])
+    assert sg["n_grad_tokens"] == n_grad
     old_pol = inst["old_host"][idx]
     W_host = to_host(inst["W"])
     t0 = time.time()
