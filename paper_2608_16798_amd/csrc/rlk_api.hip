@@ -239,7 +239,7 @@ rlk_status_t layout(const rlk_batch_t* b, bool bwd, int64_t chunk_rows, int64_t 
   if (bwd && L.nchunks < 1) L.nchunks = 1;
   L.n1 = L.nchunks;
   L.Mc1 = L.Mc2 = Mc;
-  L.g_rows = B;
+  L.g_rows = (int64_t)L.nchunks * Mc;  // every chunk Mc rows wide (row strides stay multiples of 256)
   const int64_t G = grad_tokens > 0 && grad_tokens < B ? roundup(grad_tokens, kChunkAlign) : 0;
   if (bwd && b->max_policy_tokens > 0 && G > 0 && G < B) {
     // the tokens with a gradient come first in the compacted list: chunks planned over them, then

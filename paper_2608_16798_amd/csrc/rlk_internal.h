@@ -134,7 +134,7 @@ struct WsLayout {
   SplitK sk_dwt = {1, 1};
   int64_t rows_bound = 0;          // trained tokens the chunk loop covers (N, or the caller's bound)
   // chunk c < n1 covers [c Mc1, min((c + 1) Mc1, g_rows)); the others [g_rows + (c - n1) Mc2, + Mc2)
-  // (without a hint: n1 = nchunks, Mc1 = Mc2 = Mc, g_rows = rows_bound)
+  // (without a hint: n1 = nchunks, Mc1 = Mc2 = Mc, g_rows = nchunks Mc)
   int64_t Mc1 = 0, Mc2 = 0, g_rows = 0;
   int32_t n1 = 0;
   int64_t Mc = 0;                  // chunk rows
