@@ -648,6 +648,9 @@ def test_grad_token_hint_only_plans_the_chunks():
         log(f"grad-token hint {hint} (N_grad={G}, N_eff={n_eff})")
         gpu = run_gpu(inst1, p, max_policy_tokens=n_eff)
         compare_full(inst1, gpu, ref, p, tag=f"grad hint {hint}")
+    # without the policy-token bound the hint is not used
+    p = params_for(cfg, chunk_rows=4096, grad_tokens=G)
+    compare_full(inst1, run_gpu(inst1, p), ref, p, tag="grad hint without a bound")
     pe = params_for(cfg, chunk_rows=4096, entropy_coef=0.01, grad_tokens=G)
     gpu = run_gpu(inst1, pe, max_policy_tokens=n_eff)
     compare_full(inst1, gpu, run_oracle(inst1, pe), pe, tag="grad hint with an entropy term")
