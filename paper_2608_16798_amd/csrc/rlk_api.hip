@@ -243,7 +243,9 @@ rlk_status_t layout(const rlk_batch_t* b, bool bwd, int64_t chunk_rows, int64_t 
   const int64_t G = grad_tokens > 0 && grad_tokens < B ? roundup(grad_tokens, kChunkAlign) : 0;
   if (bwd && b->max_policy_tokens > 0 && G > 0 && G < B) {
     // the tokens with a gradient come first in the compacted list: chunks planned over them, then
-    // over the rest (whose backward kernels find no rows and return).  The boundary is rounded up to
+    // over the rest (whose backward kernels, when the hint is right, find no rows and return; a
+    // wrong hint only moves work between chunks, since the kernels read the counts from the device).
+    // The boundary is rounded up to
     // whole 256-row tiles, which keeps every chunk's rows, and so the row stride of its online-LSE
     // partials, a multiple of 256.
     L.Mc1 = plan_chunk_rows(G, cap, d, L.Vp);
