@@ -195,3 +195,25 @@ def test_policy_token_bound_sizes_the_chunks(lib):
     bN = _batch(cfg, N=N, R=128)
     bN.max_policy_tokens = N
     assert rlk.workspace_size(b, p) == rlk.workspace_size(bN, p)
+
+
+def test_grad_token_hint_sizes_stay_bounded(lib):
+    # the hint re-plans the chunks of a bounded call; any value (tiny, near or past the bound, huge)
+    # gives a workspace within 1 % of the unbounded one (chunks no wider; the K-split partials of a
+    # dhidden tail may grow), and it is ignored without the bound or when the loss has another term
+    # (the sizes then equal the hint-free ones)
+    cfg = get_config("qwen8b_bf16")
+    N, bound = 524288, 211143
+    free = rlk.workspace_size(_batch(cfg, N=N, R=128), rlk.make_params())
+    b = _batch(cfg, N=N, R=128)
+    b.max_policy_tokens = bound
+    plain = rlk.workspace_size(b, rlk.make_params())
+    for hint in (1, 255, 256, 185134, bound - 1, bound, bound + 1, 1 << 62):
+        got = rlk.workspace_size(b, rlk.make_params(grad_tokens=hint))
+        assert 0 < got <= 1.01 * free, hint
+        if hint >= bound - 1:                     # rounded up to whole tiles it reaches the bound
+            assert got == plain, hint
+        assert rlk.workspace_size(b, rlk.make_params(grad_tokens=hint, entropy_coef=0.01)) == \
+            rlk.workspace_size(b, rlk.make_params(entropy_coef=0.01)), hint
+    unbounded = _batch(cfg, N=N, R=128)
+    assert rlk.workspace_size(unbounded, rlk.make_params(grad_tokens=185134)) == free
